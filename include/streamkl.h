@@ -1,0 +1,120 @@
+/*
+ * streamkl.h -- C ABI of the fused attention-distillation KL primitive for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The operation (paper Sec. 2.1, "KL Divergence"): for every batch b, head h
+ * and query row i,
+ *
+ *     S1 = s1 * Q1[b,h,i] K1[b,h]^T,   S2 = s2 * Q2[b,h,i] K2[b,h]^T,
+ *     P_t = softmax(S_t) over the keys row i may attend,
+ *     L[b,h,i] = KL(P1 || P2) = sum_j P1_j (log P1_j - log P2_j)   (eq:kl-def)
+ *
+ * computed in one online pass over key tiles (eq:kl-final, Algorithm 1) that
+ * never materialises P1 or P2, and its gradients (eq:kl-case1, eq:kl-case2,
+ * Algorithms 2 and 3) recomputed tile by tile from the saved row statistics.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - All tensor pointers are DEVICE pointers owned by the caller. The library
+ *   never allocates, frees or retains device memory, keeps no per-call state,
+ *   and never writes its inputs.
+ * - Q1, K1, Q2, K2 are bf16, contiguous, row-major:
+ *       Q1 [B, H, N_Q, d1]   K1 [B, H, N_K, d1]
+ *       Q2 [B, H, N_Q, d2]   K2 [B, H, N_K, d2]
+ *   and must be 16-byte aligned. Row statistics and gradients are fp32,
+ *   contiguous, 4-byte aligned: kl, lse1, lse2, dkl are [B, H, N_Q];
+ *   dQ1 [B,H,N_Q,d1], dQ2 [B,H,N_Q,d2], dK1 [B,H,N_K,d1], dK2 [B,H,N_K,d2].
+ * - s1, s2 are the logit scales (the paper omits sqrt(d) "for brevity"; the
+ *   usual choice is 1/sqrt(d_t)). They must be finite and > 0.
+ * - causal = 1 masks with bottom-right alignment: query row i sits at
+ *   absolute position N_K - N_Q + i and attends keys j <= that position
+ *   (j <= i when N_Q = N_K). Rows left with no key (only when N_Q > N_K)
+ *   give KL = 0, LSE = -inf and zero gradients.
+ * - direction = STREAMKL_KL_FWD evaluates KL(P1 || P2) (the paper's
+ *   objective); STREAMKL_KL_REV evaluates KL(P2 || P1). lse1/lse2 always
+ *   belong to (Q1,K1,s1) / (Q2,K2,s2).
+ * - Supported head dims: d1, d2 in {64, 128, 192, 256}.
+ * - B, H, N_Q, N_K >= 0; a zero extent is a valid call that launches
+ *   nothing (N_K = 0 with N_Q > 0 makes every row empty).
+ * - Work is enqueued on `stream` (NULL = the default stream) and the call
+ *   returns before it completes. Asynchronous faults surface at the caller's
+ *   next synchronisation, as usual for HIP.
+ * - Arguments are checked before anything is enqueued; on a non-zero return
+ *   nothing was launched (except STREAMKL_ERR_HIP, see below). No C++
+ *   exception crosses this interface. Calls on different streams are
+ *   independent and thread-safe.
+ */
+#ifndef STREAMKL_H
+#define STREAMKL_H
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  STREAMKL_OK = 0,
+  STREAMKL_ERR_INVALID_ARG = 1, /* NULL pointer, negative extent, bad flag, scale, alignment */
+  STREAMKL_ERR_UNSUPPORTED = 2, /* head dim outside {64, 128, 192, 256}, extent too large  */
+  STREAMKL_ERR_HIP = 3          /* a kernel launch was rejected by the HIP runtime          */
+} streamkl_status;
+
+typedef enum {
+  STREAMKL_KL_FWD = 0, /* L = KL(P1 || P2), eq:kl-def                */
+  STREAMKL_KL_REV = 1  /* L = KL(P2 || P1), the two roles swapped    */
+} streamkl_direction;
+
+/*
+ * Forward pass (Algorithm 1, Sec. 3.2; eq:kl-final): one tiled pass over the
+ * keys per block of query rows keeping the five running row scalars
+ * (m1, l1, m2, l2, acc). Writes, for every row,
+ *   kl   = L as defined by `direction`,
+ *   lse1 = natural-log log-sum-exp of the scaled, masked logits S1,
+ *   lse2 = the same for S2
+ * and nothing else (the saved state of Sec. 3.2, "Saved state for backward").
+ * Required: Q1, K1, Q2, K2, kl, lse1, lse2 (unless the extent is zero).
+ */
+int streamkl_fwd(const void* Q1, const void* K1, const void* Q2, const void* K2,
+                 int B, int H, int N_Q, int N_K, int d1, int d2,
+                 float s1, float s2, int causal, int direction,
+                 float* kl, float* lse1, float* lse2,
+                 hipStream_t stream);
+
+/*
+ * Backward pass (Algorithms 2 and 3, Sec. 4): recomputes S1, S2 and
+ * P_t = exp(S_t - LSE_t) tile by tile from kl/lse1/lse2 of streamkl_fwd (same
+ * inputs, scales, causal flag and direction) and returns the gradients of
+ * sum_{b,h,i} dkl[b,h,i] * L[b,h,i]:
+ *   FWD: dS2 = g (P2 - P1)                                   (eq:kl-case1)
+ *        dS1 = g P1 (r - L), r = (S1 - S2) - (LSE1 - LSE2)   (eq:kl-case2, eq:stable-r)
+ *   REV: dS1 = g (P1 - P2),  dS2 = g P2 (r' - L), r' = -r
+ *   dQ_t = s_t dS_t K_t,  dK_t = s_t dS_t^T Q_t.
+ * dkl: per-row upstream gradient g; NULL means g = 1 for every row.
+ * dQ1, dK1, dQ2, dK2: each NULL (not computed) or written in full
+ * (overwritten, never accumulated into). At least one must be non-NULL.
+ * dQ tiles are owned by query blocks and dK tiles by key blocks, so no
+ * atomics are used and results are bitwise reproducible run to run.
+ */
+int streamkl_bwd(const void* Q1, const void* K1, const void* Q2, const void* K2,
+                 int B, int H, int N_Q, int N_K, int d1, int d2,
+                 float s1, float s2, int causal, int direction,
+                 const float* kl, const float* lse1, const float* lse2,
+                 const float* dkl,
+                 float* dQ1, float* dK1, float* dQ2, float* dK2,
+                 hipStream_t stream);
+
+/* Static description of a status code. Never NULL. */
+const char* streamkl_strerror(int status);
+
+/* Library version string, e.g. "streamkl 0.1.0 gfx950". Never NULL. */
+const char* streamkl_version(void);
+
+/* 1 if d is a supported head dimension, else 0. */
+int streamkl_supported_head_dim(int d);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* STREAMKL_H */

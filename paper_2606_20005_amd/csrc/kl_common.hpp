@@ -1,0 +1,104 @@
+// Shared device helpers of the gfx950 attention-KL kernels: vector types,
+// the bf16 MFMA, the LDS tile layout and the workgroup -> tile mapping.
+//
+// Layout facts relied on throughout (v_mfma_f32_32x32x16_bf16, wave64):
+//   A operand (32 x 16):  lane l holds A[l % 32][8 * (l / 32) + 0..7]
+//   B operand (16 x 32):  lane l holds B[8 * (l / 32) + 0..7][l % 32]
+//   C result  (32 x 32):  lane l, register i holds C[8 * (i / 4) + 4 * (l / 32) + i % 4][l % 32]
+// ds_read_b64_tr_b16 (gfx950): within each group of 16 lanes, lane i receives
+//   element (i % 4) of the 8-byte pieces addressed by lanes 4 * t + i / 4,
+//   t = 0..3, so four lanes pointing at four rows of a row-major matrix
+//   deliver one column of those rows to each receiving lane.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace streamkl {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(3))) char lds_char;
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.69314718055994531f;
+constexpr float kNegInf = -__builtin_inff();
+constexpr int kXcds = 8;        // MI355X: 8 accelerator complex dies, 32 CUs each
+constexpr int kThreads = 256;   // every kernel runs 4 waves of 64 lanes
+
+__device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// 2^x on the transcendental unit (v_exp_f32); exp2(-inf) = 0.
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ f32x16 zero16() {
+  f32x16 z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = 0.f;
+  return z;
+}
+
+// ---------------------------------------------------------------------------
+// LDS tiles. A tile of R rows x D bf16 is stored as R * (D / 8) 16-byte
+// chunks, row after row, with chunk c of row r placed at slot c ^ swz(r).
+// The XOR permutes the low three chunk bits so that
+//  - eight consecutive rows read at the same chunk (MFMA operand rows) and
+//  - four consecutive rows read at two adjacent chunks (transpose reads)
+// fall on distinct 16-byte bank groups. Needs D a multiple of 64.
+// ---------------------------------------------------------------------------
+__host__ __device__ constexpr int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+
+template <int CPR>
+__device__ __forceinline__ int chunk_slot(int r, int c) { return r * CPR + (c ^ swz(r)); }
+
+// 8 consecutive bf16 (one chunk) of row r: an MFMA A/B operand.
+template <int CPR>
+__device__ __forceinline__ bf16x8 lds_row8(const uint4* tile, int r, int c) {
+  return __builtin_bit_cast(bf16x8, tile[chunk_slot<CPR>(r, c)]);
+}
+
+// Transpose read: the calling lane addresses 4 bf16 at (row r, column e),
+// e a multiple of 4; see the layout note at the top of this file.
+template <int CPR>
+__device__ __forceinline__ bf16x4 lds_tr4(const uint4* tile, int r, int e) {
+  const int byte = chunk_slot<CPR>(r, e >> 3) * 16 + ((e >> 2) & 1) * 8;
+  const lds_char* base = (const lds_char*)(tile);
+  i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + byte));
+  return __builtin_bit_cast(bf16x4, v);
+}
+
+__device__ __forceinline__ bf16x8 cat8(const bf16x4& lo, const bf16x4& hi) {
+  bf16x8 r;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) { r[t] = lo[t]; r[t + 4] = hi[t]; }
+  return r;
+}
+
+// 8 fp32 -> 8 bf16 (round to nearest even), registers first .. first + 7.
+__device__ __forceinline__ bf16x8 pack8(const float* v) {
+  bf16x8 r;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) r[t] = (__bf16)v[t];
+  return r;
+}
+
+// ---------------------------------------------------------------------------
+// Workgroup -> tile mapping. The dispatcher hands workgroup w to XCD w % 8,
+// and each XCD has its own L2. Renumber so that XCD x receives a contiguous
+// range of logical tiles: the workgroups resident on one XCD then belong to
+// the same (batch, head) and stream the same key tiles through its L2.
+// Bijective for any grid size.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int xcd_logical(int bid, int nb) {
+  const int q = nb / kXcds, r = nb % kXcds;
+  const int x = bid % kXcds, k = bid / kXcds;
+  return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + k;
+}
+
+}  // namespace streamkl

@@ -1,0 +1,48 @@
+// Internal launch interface between the C ABI (streamkl_api.hip) and the
+// translation units that instantiate the kernels for each head-dim pair.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace streamkl {
+
+// Arguments after the host has resolved the KL direction: "a" is the
+// distribution in the first KL slot, "b" the one in the second.
+struct FwdArgs {
+  const uint16_t *Qa, *Ka, *Qb, *Kb;
+  int BH, NQ, NK;
+  float ca, cb;                 // s * log2(e)
+  float *kl, *lse_a, *lse_b;
+  hipStream_t stream;
+};
+
+struct BwdArgs {
+  const uint16_t *Qa, *Ka, *Qb, *Kb;
+  int BH, NQ, NK;
+  float sa, sb;
+  const float *kl, *lse_a, *lse_b, *g;
+  float *dQa, *dQb, *dKa, *dKb;
+  hipStream_t stream;
+};
+
+// Each returns hipErrorInvalidValue for a head-dim pair it does not hold,
+// otherwise the status of the launch (hipGetLastError).
+hipError_t launch_fwd(int da, int db, bool causal, const FwdArgs& a);
+hipError_t launch_bwd_dq(int da, int db, bool causal, int mode, const BwdArgs& a);
+hipError_t launch_bwd_dk(int da, int db, bool causal, int mode, const BwdArgs& a);
+hipError_t launch_bwd_dq_m1(int da, int db, bool causal, const BwdArgs& a);
+hipError_t launch_bwd_dq_m2(int da, int db, bool causal, const BwdArgs& a);
+hipError_t launch_bwd_dq_m3(int da, int db, bool causal, const BwdArgs& a);
+hipError_t launch_bwd_dk_m1(int da, int db, bool causal, const BwdArgs& a);
+hipError_t launch_bwd_dk_m2(int da, int db, bool causal, const BwdArgs& a);
+hipError_t launch_bwd_dk_m3(int da, int db, bool causal, const BwdArgs& a);
+
+// Expands F(DA, DB) for every supported head-dim pair.
+#define STREAMKL_FOR_EACH_DIM_PAIR(F)                                        \
+  F(64, 64) F(64, 128) F(64, 192) F(64, 256)                                 \
+  F(128, 64) F(128, 128) F(128, 192) F(128, 256)                             \
+  F(192, 64) F(192, 128) F(192, 192) F(192, 256)                             \
+  F(256, 64) F(256, 128) F(256, 192) F(256, 256)
+
+}  // namespace streamkl

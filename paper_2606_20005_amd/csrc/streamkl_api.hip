@@ -1,0 +1,181 @@
+// C ABI of the attention-KL library: argument checking, resolution of the
+// KL direction into (first slot, second slot) roles, and kernel dispatch.
+// Every check happens before anything is enqueued, and no HIP call is made
+// on an error path, so the checks are exercised on hosts without a GPU.
+#include <cmath>
+#include <cstdint>
+
+#include "kl_launch.hpp"
+#include "streamkl.h"
+
+namespace {
+
+using streamkl::BwdArgs;
+using streamkl::FwdArgs;
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr long long kMaxGrid = 0x7fffffffLL;
+
+bool supported_dim(int d) { return d == 64 || d == 128 || d == 192 || d == 256; }
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+bool scale_ok(float s) { return std::isfinite(s) && s > 0.f; }
+
+// Checks shared by both passes. Returns STREAMKL_OK or an error code.
+int check_common(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H, int N_Q,
+                 int N_K, int d1, int d2, float s1, float s2, int causal, int direction, bool* empty) {
+  if (B < 0 || H < 0 || N_Q < 0 || N_K < 0) return STREAMKL_ERR_INVALID_ARG;
+  if (causal != 0 && causal != 1) return STREAMKL_ERR_INVALID_ARG;
+  if (direction != STREAMKL_KL_FWD && direction != STREAMKL_KL_REV) return STREAMKL_ERR_INVALID_ARG;
+  if (!scale_ok(s1) || !scale_ok(s2)) return STREAMKL_ERR_INVALID_ARG;
+  if (!supported_dim(d1) || !supported_dim(d2)) return STREAMKL_ERR_UNSUPPORTED;
+  const long long bh = (long long)B * H;
+  if (bh > kMaxGrid) return STREAMKL_ERR_UNSUPPORTED;
+  // one workgroup per 128 rows of one head; element offsets are 64-bit in the kernels
+  if (bh * ((N_Q + 127LL) / 128) > kMaxGrid || bh * ((N_K + 127LL) / 128) > kMaxGrid)
+    return STREAMKL_ERR_UNSUPPORTED;
+  *empty = bh == 0 || N_Q == 0;
+  if (*empty) return STREAMKL_OK;
+  if (!Q1 || !Q2) return STREAMKL_ERR_INVALID_ARG;
+  if (N_K > 0 && (!K1 || !K2)) return STREAMKL_ERR_INVALID_ARG;
+  if (!aligned(Q1, 16) || !aligned(Q2, 16) || (K1 && !aligned(K1, 16)) || (K2 && !aligned(K2, 16)))
+    return STREAMKL_ERR_INVALID_ARG;
+  return STREAMKL_OK;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? STREAMKL_OK : STREAMKL_ERR_HIP; }
+
+// Zero fill by a kernel rather than hipMemsetAsync, so that the call stays
+// safe to record into a HIP graph.
+__global__ void zero_fill_kernel(float* __restrict__ p, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = 0.f;
+}
+
+hipError_t zero_fill(float* p, size_t n, hipStream_t stream) {
+  if (!p || n == 0) return hipSuccess;
+  const size_t blocks = (n + 255) / 256;
+  hipLaunchKernelGGL(zero_fill_kernel, dim3((unsigned)(blocks < 4096 ? blocks : 4096)), dim3(256), 0, stream, p, n);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+extern "C" int streamkl_fwd(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H, int N_Q,
+                            int N_K, int d1, int d2, float s1, float s2, int causal, int direction, float* kl,
+                            float* lse1, float* lse2, hipStream_t stream) {
+  bool empty = false;
+  const int st = check_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, &empty);
+  if (st != STREAMKL_OK || empty) return st;
+  if (!kl || !lse1 || !lse2) return STREAMKL_ERR_INVALID_ARG;
+  if (!aligned(kl, 4) || !aligned(lse1, 4) || !aligned(lse2, 4)) return STREAMKL_ERR_INVALID_ARG;
+  const bool rev = direction == STREAMKL_KL_REV;
+  FwdArgs a;
+  a.Qa = static_cast<const uint16_t*>(rev ? Q2 : Q1);
+  a.Ka = static_cast<const uint16_t*>(rev ? K2 : K1);
+  a.Qb = static_cast<const uint16_t*>(rev ? Q1 : Q2);
+  a.Kb = static_cast<const uint16_t*>(rev ? K1 : K2);
+  a.BH = B * H;
+  a.NQ = N_Q;
+  a.NK = N_K;
+  a.ca = (rev ? s2 : s1) * kLog2e;
+  a.cb = (rev ? s1 : s2) * kLog2e;
+  a.kl = kl;
+  a.lse_a = rev ? lse2 : lse1;
+  a.lse_b = rev ? lse1 : lse2;
+  a.stream = stream;
+  return hip_status(streamkl::launch_fwd(rev ? d2 : d1, rev ? d1 : d2, causal == 1, a));
+}
+
+extern "C" int streamkl_bwd(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H, int N_Q,
+                            int N_K, int d1, int d2, float s1, float s2, int causal, int direction,
+                            const float* kl, const float* lse1, const float* lse2, const float* dkl, float* dQ1,
+                            float* dK1, float* dQ2, float* dK2, hipStream_t stream) {
+  if (!dQ1 && !dK1 && !dQ2 && !dK2) return STREAMKL_ERR_INVALID_ARG;
+  bool empty = false;
+  int st = check_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, &empty);
+  if (st != STREAMKL_OK) return st;
+  const long long bh = (long long)B * H;
+  // With N_Q = 0 every dK is zero and there is no dQ; with N_K = 0 every dQ is zero.
+  if (bh == 0) return STREAMKL_OK;
+  if (N_Q == 0) {
+    if ((dK1 && !aligned(dK1, 4)) || (dK2 && !aligned(dK2, 4))) return STREAMKL_ERR_INVALID_ARG;
+    hipError_t e = hipSuccess;
+    e = zero_fill(dK1, (size_t)bh * N_K * d1, stream);
+    if (e == hipSuccess) e = zero_fill(dK2, (size_t)bh * N_K * d2, stream);
+    return hip_status(e);
+  }
+  if (!kl || !lse1 || !lse2) return STREAMKL_ERR_INVALID_ARG;
+  const void* ptrs[] = {kl, lse1, lse2, dkl, dQ1, dK1, dQ2, dK2};
+  for (const void* p : ptrs)
+    if (p && !aligned(p, 4)) return STREAMKL_ERR_INVALID_ARG;
+  const bool rev = direction == STREAMKL_KL_REV;
+  BwdArgs a;
+  a.Qa = static_cast<const uint16_t*>(rev ? Q2 : Q1);
+  a.Ka = static_cast<const uint16_t*>(rev ? K2 : K1);
+  a.Qb = static_cast<const uint16_t*>(rev ? Q1 : Q2);
+  a.Kb = static_cast<const uint16_t*>(rev ? K1 : K2);
+  a.BH = (int)bh;
+  a.NQ = N_Q;
+  a.NK = N_K;
+  a.sa = rev ? s2 : s1;
+  a.sb = rev ? s1 : s2;
+  a.kl = kl;
+  a.lse_a = rev ? lse2 : lse1;
+  a.lse_b = rev ? lse1 : lse2;
+  a.g = dkl;
+  a.dQa = rev ? dQ2 : dQ1;
+  a.dQb = rev ? dQ1 : dQ2;
+  a.dKa = rev ? dK2 : dK1;
+  a.dKb = rev ? dK1 : dK2;
+  a.stream = stream;
+  const int da = rev ? d2 : d1, db = rev ? d1 : d2;
+  const int mode_q = (a.dQb ? 1 : 0) | (a.dQa ? 2 : 0);
+  const int mode_k = (a.dKb ? 1 : 0) | (a.dKa ? 2 : 0);
+  hipError_t e = hipSuccess;
+  if (mode_q) {
+    if (N_K == 0) {   // every row is empty: zero gradients
+      e = zero_fill(a.dQa, (size_t)bh * N_Q * da, stream);
+      if (e == hipSuccess) e = zero_fill(a.dQb, (size_t)bh * N_Q * db, stream);
+    } else {
+      e = streamkl::launch_bwd_dq(da, db, causal == 1, mode_q, a);
+    }
+  }
+  if (e == hipSuccess && mode_k && N_K > 0) e = streamkl::launch_bwd_dk(da, db, causal == 1, mode_k, a);
+  return hip_status(e);
+}
+
+extern "C" const char* streamkl_strerror(int status) {
+  switch (status) {
+    case STREAMKL_OK: return "success";
+    case STREAMKL_ERR_INVALID_ARG: return "invalid argument (null pointer, negative extent, flag, scale or alignment)";
+    case STREAMKL_ERR_UNSUPPORTED: return "unsupported configuration (head dim not in {64,128,192,256} or extent too large)";
+    case STREAMKL_ERR_HIP: return "HIP runtime rejected a kernel launch";
+    default: return "unknown status";
+  }
+}
+
+extern "C" const char* streamkl_version(void) { return "streamkl 0.1.0 gfx950"; }
+
+extern "C" int streamkl_supported_head_dim(int d) { return supported_dim(d) ? 1 : 0; }
+
+namespace streamkl {
+
+hipError_t launch_bwd_dq(int da, int db, bool causal, int mode, const BwdArgs& a) {
+  switch (mode) {
+    case 1: return launch_bwd_dq_m1(da, db, causal, a);
+    case 2: return launch_bwd_dq_m2(da, db, causal, a);
+    case 3: return launch_bwd_dq_m3(da, db, causal, a);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_bwd_dk(int da, int db, bool causal, int mode, const BwdArgs& a) {
+  switch (mode) {
+    case 1: return launch_bwd_dk_m1(da, db, causal, a);
+    case 2: return launch_bwd_dk_m2(da, db, causal, a);
+    case 3: return launch_bwd_dk_m3(da, db, causal, a);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace streamkl

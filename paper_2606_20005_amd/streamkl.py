@@ -1,0 +1,200 @@
+"""Python binding of libstreamkl.so (the C ABI declared in include/streamkl.h).
+
+Argument marshalling only: every step of the forward and backward pass runs
+in the library's gfx950 kernels. PyTorch provides device memory and the
+current HIP stream. Importing this module fails loudly when the library has
+not been built; there is no fallback implementation.
+
+    kl, lse1, lse2 = fwd(q1, k1, q2, k2, s1, s2, causal, direction)
+    dQ1, dK1, dQ2, dK2 = bwd(q1, k1, q2, k2, kl, lse1, lse2, dkl, ..., want=("dq2", "dk2"))
+    loss = attention_kl(q1, k1, q2, k2, causal=True).mean(); loss.backward()
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libstreamkl.so")
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP = 0, 1, 2, 3
+FWD, REV = 0, 1
+ENTRY_POINTS = ("streamkl_fwd", "streamkl_bwd", "streamkl_strerror", "streamkl_version",
+                "streamkl_supported_head_dim")
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2606_20005_amd.build` "
+                          "(the attention-KL primitive has no non-HIP implementation)")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i, f = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
+    lib.streamkl_fwd.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, f, f, i, i, vp, vp, vp, vp]
+    lib.streamkl_fwd.restype = i
+    lib.streamkl_bwd.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, f, f, i, i, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.streamkl_bwd.restype = i
+    lib.streamkl_strerror.argtypes = [i]
+    lib.streamkl_strerror.restype = ctypes.c_char_p
+    lib.streamkl_version.argtypes = []
+    lib.streamkl_version.restype = ctypes.c_char_p
+    lib.streamkl_supported_head_dim.argtypes = [i]
+    lib.streamkl_supported_head_dim.restype = i
+    return lib
+
+
+lib = _load()
+
+
+class StreamKLError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {lib.streamkl_strerror(status).decode()} (status {status})")
+
+
+def version() -> str:
+    return lib.streamkl_version().decode()
+
+
+def supported_head_dim(d: int) -> bool:
+    return bool(lib.streamkl_supported_head_dim(int(d)))
+
+
+def _p(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(dev):
+    return ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+
+
+def _direction(direction) -> int:
+    if direction in (FWD, "fwd", "forward"):
+        return FWD
+    if direction in (REV, "rev", "reverse"):
+        return REV
+    raise ValueError(f"direction must be 'fwd' (KL(P1||P2)) or 'rev' (KL(P2||P1)), got {direction!r}")
+
+
+def _check_inputs(q1, k1, q2, k2):
+    for n, t in (("q1", q1), ("k1", k1), ("q2", q2), ("k2", k2)):
+        if not isinstance(t, torch.Tensor) or not t.is_cuda:
+            raise ValueError(f"{n} must be a GPU tensor")
+        if t.dtype != torch.bfloat16:
+            raise ValueError(f"{n} must be bfloat16, got {t.dtype}")
+        if t.dim() != 4 or not t.is_contiguous():
+            raise ValueError(f"{n} must be a contiguous [B, H, N, d] tensor")
+    B, H, NQ, d1 = q1.shape
+    NK = k1.shape[2]
+    d2 = q2.shape[3]
+    if tuple(k1.shape) != (B, H, NK, d1) or tuple(q2.shape) != (B, H, NQ, d2) or tuple(k2.shape) != (B, H, NK, d2):
+        raise ValueError(f"inconsistent shapes q1{tuple(q1.shape)} k1{tuple(k1.shape)} "
+                         f"q2{tuple(q2.shape)} k2{tuple(k2.shape)}")
+    if len({q1.device, k1.device, q2.device, k2.device}) != 1:
+        raise ValueError("all inputs must be on one device")
+    return B, H, NQ, NK, d1, d2
+
+
+def _scales(s1, s2, d1, d2):
+    return (1.0 / math.sqrt(d1) if s1 is None else float(s1)), (1.0 / math.sqrt(d2) if s2 is None else float(s2))
+
+
+def _f32_rows(t, shape, dev, name):
+    if t is None:
+        return None
+    if t.dtype != torch.float32 or tuple(t.shape) != shape or not t.is_contiguous() or t.device != dev:
+        raise ValueError(f"{name} must be a contiguous float32 tensor of shape {shape} on {dev}")
+    return t
+
+
+def fwd(q1, k1, q2, k2, s1=None, s2=None, causal=False, direction=FWD, out=None):
+    """streamkl_fwd: returns (kl, lse1, lse2), float32 [B, H, N_Q].
+
+    s_t defaults to 1/sqrt(d_t). ``out`` may hold three preallocated tensors.
+    """
+    B, H, NQ, NK, d1, d2 = _check_inputs(q1, k1, q2, k2)
+    s1, s2 = _scales(s1, s2, d1, d2)
+    dev = q1.device
+    if out is None:
+        out = tuple(torch.empty((B, H, NQ), dtype=torch.float32, device=dev) for _ in range(3))
+    kl, lse1, lse2 = (_f32_rows(t, (B, H, NQ), dev, n) for t, n in zip(out, ("kl", "lse1", "lse2")))
+    with torch.cuda.device(dev):
+        st = lib.streamkl_fwd(_p(q1), _p(k1), _p(q2), _p(k2), B, H, NQ, NK, d1, d2, s1, s2,
+                              int(bool(causal)), _direction(direction), _p(kl), _p(lse1), _p(lse2), _stream(dev))
+    if st != OK:
+        raise StreamKLError(st, "streamkl_fwd")
+    return kl, lse1, lse2
+
+
+def bwd(q1, k1, q2, k2, kl, lse1, lse2, dkl=None, s1=None, s2=None, causal=False, direction=FWD,
+        want=("dq2", "dk2"), out=None):
+    """streamkl_bwd: returns (dQ1, dK1, dQ2, dK2), float32, None where not requested.
+
+    want: any of "dq1", "dk1", "dq2", "dk2". dkl: per-row upstream gradient
+    (float32 [B, H, N_Q]) or None for all ones. ``out`` may map those names to
+    preallocated tensors.
+    """
+    B, H, NQ, NK, d1, d2 = _check_inputs(q1, k1, q2, k2)
+    s1, s2 = _scales(s1, s2, d1, d2)
+    dev = q1.device
+    rows = (B, H, NQ)
+    kl, lse1, lse2 = (_f32_rows(t, rows, dev, n) for t, n in ((kl, "kl"), (lse1, "lse1"), (lse2, "lse2")))
+    dkl = _f32_rows(dkl, rows, dev, "dkl")
+    shapes = {"dq1": (B, H, NQ, d1), "dk1": (B, H, NK, d1), "dq2": (B, H, NQ, d2), "dk2": (B, H, NK, d2)}
+    unknown = set(want) - set(shapes)
+    if unknown:
+        raise ValueError(f"unknown gradient names {sorted(unknown)}")
+    out = dict(out or {})
+    grads = {}
+    for n in ("dq1", "dk1", "dq2", "dk2"):
+        if n in want:
+            t = out.get(n)
+            grads[n] = _f32_rows(t, shapes[n], dev, n) if t is not None else \
+                torch.empty(shapes[n], dtype=torch.float32, device=dev)
+        else:
+            grads[n] = None
+    with torch.cuda.device(dev):
+        st = lib.streamkl_bwd(_p(q1), _p(k1), _p(q2), _p(k2), B, H, NQ, NK, d1, d2, s1, s2,
+                              int(bool(causal)), _direction(direction), _p(kl), _p(lse1), _p(lse2), _p(dkl),
+                              _p(grads["dq1"]), _p(grads["dk1"]), _p(grads["dq2"]), _p(grads["dk2"]),
+                              _stream(dev))
+    if st != OK:
+        raise StreamKLError(st, "streamkl_bwd")
+    return grads["dq1"], grads["dk1"], grads["dq2"], grads["dk2"]
+
+
+class _AttentionKL(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, q1, k1, q2, k2, s1, s2, causal, direction):
+        kl, lse1, lse2 = fwd(q1, k1, q2, k2, s1, s2, causal, direction)
+        ctx.save_for_backward(q1, k1, q2, k2, kl, lse1, lse2)
+        ctx.cfg = (s1, s2, causal, direction)
+        ctx.mark_non_differentiable(lse1, lse2)
+        return kl, lse1, lse2
+
+    @staticmethod
+    def backward(ctx, gkl, _glse1, _glse2):
+        q1, k1, q2, k2, kl, lse1, lse2 = ctx.saved_tensors
+        s1, s2, causal, direction = ctx.cfg
+        names = [n for n, need in zip(("dq1", "dk1", "dq2", "dk2"), ctx.needs_input_grad[:4]) if need]
+        if not names:
+            return (None,) * 8
+        g = gkl.to(torch.float32).contiguous()
+        dq1, dk1, dq2, dk2 = bwd(q1, k1, q2, k2, kl, lse1, lse2, g, s1, s2, causal, direction, want=names)
+        cast = lambda t, ref: None if t is None else t.to(ref.dtype)   # noqa: E731
+        return cast(dq1, q1), cast(dk1, k1), cast(dq2, q2), cast(dk2, k2), None, None, None, None
+
+
+def attention_kl(q1, k1, q2, k2, *, s1=None, s2=None, causal=False, direction="fwd", return_lse=False):
+    """Per-row KL between softmax(s1 q1 k1^T) and softmax(s2 q2 k2^T), differentiable.
+
+    Returns kl [B, H, N_Q] (and lse1, lse2 if ``return_lse``). The paper's
+    training objective is ``attention_kl(...).mean()``. Gradients flow to the
+    inputs that require them: (q2, k2) in standard distillation (Setting 1),
+    (q1, k1) when the first distribution is trained (Setting 2), or both.
+    """
+    d1, d2 = q1.shape[-1], q2.shape[-1]
+    s1, s2 = _scales(s1, s2, d1, d2)
+    kl, lse1, lse2 = _AttentionKL.apply(q1, k1, q2, k2, s1, s2, bool(causal), _direction(direction))
+    return (kl, lse1, lse2) if return_lse else kl

@@ -1,0 +1,97 @@
+"""The C-ABI library loads on a host without a GPU, exports every entry point
+declared in include/streamkl.h, and rejects bad arguments before enqueuing
+anything (no compute call is made here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "streamkl.h")
+
+
+@pytest.fixture(scope="module")
+def sk():
+    from paper_2606_20005_amd import streamkl
+    return streamkl
+
+
+def declared_entry_points():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(streamkl_\w+)\s*\(", text)))
+
+
+def test_header_declares_expected_entry_points(sk):
+    assert declared_entry_points() == sorted(sk.ENTRY_POINTS)
+
+
+def test_library_exports_every_declared_symbol(sk):
+    for name in declared_entry_points():
+        assert hasattr(sk.lib, name), name
+
+
+def test_version_and_strerror(sk):
+    assert sk.version().startswith("streamkl ") and "gfx950" in sk.version()
+    for st in range(4):
+        assert sk.lib.streamkl_strerror(st)
+    assert b"unknown" in sk.lib.streamkl_strerror(99)
+    assert [d for d in range(0, 300) if sk.supported_head_dim(d)] == [64, 128, 192, 256]
+
+
+FAKE = ctypes.c_void_p(0x100000)        # 16-byte aligned, never dereferenced on error paths
+MIS = ctypes.c_void_p(0x100008)         # 8-byte aligned only
+
+
+def fwd_call(sk, **kw):
+    a = dict(Q1=FAKE, K1=FAKE, Q2=FAKE, K2=FAKE, B=1, H=2, NQ=64, NK=64, d1=64, d2=64, s1=0.125, s2=0.125,
+             causal=0, direction=0, kl=FAKE, lse1=FAKE, lse2=FAKE, stream=None)
+    a.update(kw)
+    return sk.lib.streamkl_fwd(a["Q1"], a["K1"], a["Q2"], a["K2"], a["B"], a["H"], a["NQ"], a["NK"], a["d1"],
+                               a["d2"], a["s1"], a["s2"], a["causal"], a["direction"], a["kl"], a["lse1"],
+                               a["lse2"], a["stream"])
+
+
+def bwd_call(sk, **kw):
+    a = dict(Q1=FAKE, K1=FAKE, Q2=FAKE, K2=FAKE, B=1, H=2, NQ=64, NK=64, d1=64, d2=64, s1=0.125, s2=0.125,
+             causal=0, direction=0, kl=FAKE, lse1=FAKE, lse2=FAKE, dkl=None, dQ1=None, dK1=None, dQ2=FAKE,
+             dK2=FAKE, stream=None)
+    a.update(kw)
+    return sk.lib.streamkl_bwd(a["Q1"], a["K1"], a["Q2"], a["K2"], a["B"], a["H"], a["NQ"], a["NK"], a["d1"],
+                               a["d2"], a["s1"], a["s2"], a["causal"], a["direction"], a["kl"], a["lse1"],
+                               a["lse2"], a["dkl"], a["dQ1"], a["dK1"], a["dQ2"], a["dK2"], a["stream"])
+
+
+@pytest.mark.parametrize("call", [fwd_call, bwd_call])
+@pytest.mark.parametrize("kw,expect", [
+    (dict(Q1=None), 1), (dict(K2=None), 1), (dict(kl=None), 1), (dict(lse2=None), 1),
+    (dict(B=-1), 1), (dict(NQ=-3), 1), (dict(NK=-1), 1), (dict(causal=2), 1), (dict(direction=5), 1),
+    (dict(s1=0.0), 1), (dict(s2=-0.5), 1), (dict(s1=float("inf")), 1), (dict(s2=float("nan")), 1),
+    (dict(Q1=MIS), 1), (dict(K1=MIS), 1),
+    (dict(d1=96), 2), (dict(d2=32), 2), (dict(d1=512), 2), (dict(B=70000, H=70000), 2),
+    (dict(B=0), 0), (dict(H=0), 0), (dict(NQ=0, Q1=None, Q2=None, kl=None, lse1=None, lse2=None,
+                                          dQ2=None, dK2=None, dK1=FAKE), None),
+])
+def test_argument_checks(sk, call, kw, expect):
+    if expect is None:          # N_Q = 0: forward is a no-op; backward would zero-fill dK (a launch)
+        if call is fwd_call:
+            assert call(sk, **kw) == 0
+        return
+    assert call(sk, **kw) == expect
+
+
+def test_bwd_needs_one_gradient(sk):
+    assert bwd_call(sk, dQ2=None, dK2=None) == 1
+
+
+def test_bwd_misaligned_fp32(sk):
+    assert bwd_call(sk, dQ2=ctypes.c_void_p(0x100002)) == 1
+    assert bwd_call(sk, dkl=ctypes.c_void_p(0x100001)) == 1
+
+
+def test_python_binding_rejects_cpu_tensors(sk):
+    import torch
+    x = torch.zeros((1, 1, 4, 64), dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        sk.fwd(x, x, x, x)

@@ -1,0 +1,168 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle, element
+by element, on identical seeded bf16 inputs, at sizes that span several tiles
+and a ragged tail. Full-size workloads are in test_gpu_fullsize.py."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_20005_amd import inputs
+from parity_utils import check_grad, check_rows, to_gpu_f32, upload
+
+pytestmark = pytest.mark.gpu
+
+ALL = ("dq1", "dk1", "dq2", "dk2")
+
+
+def run_case(sk, d, causal, direction, want=ALL, use_g=True):
+    import torch
+    w = d["w"]
+    q1, k1, q2, k2 = upload(d)
+    kl, l1, l2 = sk.fwd(q1, k1, q2, k2, w.s1, w.s2, causal, direction)
+    g_np = d["g"] if use_g else None
+    g = to_gpu_f32(g_np) if use_g else None
+    grads = sk.bwd(q1, k1, q2, k2, kl, l1, l2, g, w.s1, w.s2, causal, direction, want=want)
+    torch.cuda.synchronize()
+    ref = oracle.backward(d["Q1"], d["K1"], d["Q2"], d["K2"], w.s1, w.s2, causal, direction, g_np)
+    check_rows("kl", kl.cpu().numpy(), ref[0])
+    check_rows("lse1", l1.cpu().numpy(), ref[1])
+    check_rows("lse2", l2.cpu().numpy(), ref[2])
+    out = {}
+    for name, got, r in zip(ALL, grads, ref[3:]):
+        if name in want:
+            out[name] = check_grad(name, got.cpu().numpy(), r)
+        else:
+            assert got is None
+    return out
+
+
+@pytest.mark.parametrize("direction", [0, 1])
+@pytest.mark.parametrize("causal", [False, True])
+def test_tiny_all_outputs(gpu_lib, causal, direction):
+    run_case(gpu_lib, inputs.make("tiny"), causal, direction)
+
+
+def test_tiny_identical_exact_zero(gpu_lib):
+    import torch
+    d = inputs.make("tiny", "identical")
+    w = d["w"]
+    q1, k1, q2, k2 = upload(d)
+    for causal in (False, True):
+        kl, l1, l2 = gpu_lib.fwd(q1, k1, q2, k2, w.s1, w.s2, causal, 0)
+        grads = gpu_lib.bwd(q1, k1, q2, k2, kl, l1, l2, None, w.s1, w.s2, causal, 0, want=ALL)
+        torch.cuda.synchronize()
+        assert float(kl.abs().max()) <= 1e-6
+        for t in grads:
+            assert float(t.abs().max()) <= 1e-6
+
+
+def test_tiny_q1_zero_uniform(gpu_lib):
+    for causal in (False, True):
+        run_case(gpu_lib, inputs.make("tiny", "q1zero"), causal, 0)
+
+
+@pytest.mark.parametrize("nq,nk,causal", [
+    (257, 257, False), (257, 257, True), (1000, 1000, True), (100, 300, True), (100, 300, False),
+    (300, 100, True), (1, 1, False), (1, 200, True), (129, 33, False), (33, 129, True), (64, 1, True),
+])
+def test_ragged_shapes(gpu_lib, nq, nk, causal):
+    d = inputs.make("tiny", B=1, H=2, n_q=nq, n_k=nk)
+    run_case(gpu_lib, d, causal, 0)
+
+
+@pytest.mark.parametrize("d1", [64, 128, 192, 256])
+@pytest.mark.parametrize("d2", [64, 128, 192, 256])
+def test_every_head_dim_pair(gpu_lib, d1, d2):
+    d = inputs.make("tiny", B=1, H=1, n_q=160, n_k=200, d1=d1, d2=d2, s1=d1 ** -0.5, s2=d2 ** -0.5)
+    run_case(gpu_lib, d, True, 0)
+    run_case(gpu_lib, d, False, 1)
+
+
+@pytest.mark.parametrize("want", [("dq2", "dk2"), ("dq1", "dk1"), ("dq2",), ("dk1",), ("dq1", "dk2")])
+@pytest.mark.parametrize("direction", [0, 1])
+def test_gradient_subsets(gpu_lib, want, direction):
+    d = inputs.make("tiny", B=1, H=1, n_q=200, n_k=230, d1=128, d2=64, s1=128 ** -0.5)
+    run_case(gpu_lib, d, True, direction, want=want)
+
+
+def test_upstream_gradient_none_is_ones(gpu_lib):
+    run_case(gpu_lib, inputs.make("tiny", n_q=130, n_k=190), True, 0, use_g=False)
+
+
+@pytest.mark.parametrize("name,over,causal", [
+    ("distill", dict(H=2, n_q=512, n_k=512), True),
+    ("mid", dict(H=2, n_q=512, n_k=512), False),
+    ("mid", dict(H=2, n_q=512, n_k=512), True),
+    ("long", dict(H=2, n_q=640, n_k=640), True),
+    ("indexer", dict(H=2, n_q=128, n_k=2048), True),
+])
+def test_workload_structures_reduced(gpu_lib, name, over, causal):
+    """Each workload's value distribution and masking at a size the full oracle covers."""
+    run_case(gpu_lib, inputs.make(name, **over), causal, 0)
+
+
+def test_deterministic_and_inputs_untouched(gpu_lib):
+    import torch
+    d = inputs.make("distill", H=2, n_q=384, n_k=384)
+    w = d["w"]
+    q1, k1, q2, k2 = upload(d)
+    before = [t.clone() for t in (q1, k1, q2, k2)]
+    runs = []
+    for _ in range(2):
+        kl, l1, l2 = gpu_lib.fwd(q1, k1, q2, k2, w.s1, w.s2, True, 0)
+        g = gpu_lib.bwd(q1, k1, q2, k2, kl, l1, l2, None, w.s1, w.s2, True, 0, want=ALL)
+        torch.cuda.synchronize()
+        runs.append([t.cpu() for t in (kl, l1, l2, *g)])
+    for a, b in zip(*runs):
+        assert torch.equal(a, b)
+    for a, b in zip(before, (q1, k1, q2, k2)):
+        assert torch.equal(a, b)
+
+
+def test_no_device_allocation_in_library(gpu_lib):
+    import torch
+    d = inputs.make("tiny", n_q=512, n_k=512)
+    w = d["w"]
+    q1, k1, q2, k2 = upload(d)
+    kl, l1, l2 = (torch.empty((1, 1, 512), dtype=torch.float32, device="cuda") for _ in range(3))
+    grads = {n: torch.empty((1, 1, 512, 64), dtype=torch.float32, device="cuda") for n in ALL}
+    gpu_lib.fwd(q1, k1, q2, k2, w.s1, w.s2, True, 0, out=(kl, l1, l2))
+    torch.cuda.synchronize()
+    free0, _ = torch.cuda.mem_get_info()
+    alloc0 = torch.cuda.memory_allocated()
+    for _ in range(3):
+        gpu_lib.fwd(q1, k1, q2, k2, w.s1, w.s2, True, 0, out=(kl, l1, l2))
+        gpu_lib.bwd(q1, k1, q2, k2, kl, l1, l2, None, w.s1, w.s2, True, 0, want=ALL, out=grads)
+    torch.cuda.synchronize()
+    free1, _ = torch.cuda.mem_get_info()
+    assert torch.cuda.memory_allocated() == alloc0
+    assert free1 == free0
+
+
+def test_autograd_mean_objective(gpu_lib):
+    """loss = mean over (b, h, i) of KL (the paper's objective); grads of q2, k2 only."""
+    import torch
+    d = inputs.make("distill", H=2, n_q=256, n_k=256)
+    w = d["w"]
+    q1, k1, q2, k2 = upload(d)
+    q2.requires_grad_(True)
+    k2.requires_grad_(True)
+    kl = gpu_lib.attention_kl(q1, k1, q2, k2, s1=w.s1, s2=w.s2, causal=True)
+    loss = kl.mean()
+    loss.backward()
+    torch.cuda.synchronize()
+    n = kl.numel()
+    ref = oracle.backward(d["Q1"], d["K1"], d["Q2"], d["K2"], w.s1, w.s2, True, 0, np.full(kl.shape, 1.0 / n))
+    check_rows("kl", kl.detach().cpu().numpy(), ref[0])
+    assert q1.grad is None and k1.grad is None
+    # the autograd path returns bf16 gradients (the input dtype)
+    check_grad("dq2", q2.grad.float().cpu().numpy(), ref[5])
+    check_grad("dk2", k2.grad.float().cpu().numpy(), ref[6])
+
+
+def test_invalid_arguments_raise(gpu_lib):
+    d = inputs.make("tiny", n_q=64, n_k=64)
+    q1, k1, q2, k2 = upload(d)
+    with pytest.raises(gpu_lib.StreamKLError):
+        gpu_lib.fwd(q1, k1, q2, k2, -1.0, 0.1)
+    with pytest.raises(ValueError):
+        gpu_lib.fwd(q1.float(), k1, q2, k2)
