@@ -32,15 +32,14 @@ struct BwdCfg {
   static constexpr int BS = 32;                          // streamed rows per tile
   static constexpr int CA = DA / 8, CB = DB / 8;
   static constexpr int STAGE = BS * (CA + CB);           // chunks per LDS stage
-  static constexpr int CHT = STAGE / kThreads;
-  static constexpr int CHT_A = BS * CA / kThreads;
   static constexpr bool WANT_B = (MODE & 1) != 0;
   static constexpr bool WANT_A = (MODE & 2) != 0;
-  // register estimate: resident operands + two logit tiles + gradient tiles
-  static constexpr int REGS = (DA + DB) / 4 + 32 + (WANT_A ? DA / 2 : 0) + (WANT_B ? DB / 2 : 0) + CHT * 4;
-  static constexpr int MINB = REGS <= 176 ? 2 : 1;
+  // register estimate per lane: resident operands + two logit tiles + gradient
+  // tiles + about 80 for operands in flight, addresses and row statistics;
+  // two waves per SIMD leave 256.
+  static constexpr int REGS = (DA + DB) / 4 + 32 + (WANT_A ? DA / 2 : 0) + (WANT_B ? DB / 2 : 0) + 80;
+  static constexpr int MINB = REGS <= 248 ? 2 : 1;
   static_assert(DA % 64 == 0 && DB % 64 == 0, "head dims must be multiples of 64");
-  static_assert(STAGE % kThreads == 0 && (BS * CA) % kThreads == 0, "staging split");
   static_assert(MODE >= 1 && MODE <= 3, "at least one gradient");
 };
 
@@ -73,14 +72,102 @@ __device__ __forceinline__ void dlogits(float ra, float rb, bool ok, float ca, f
                                         const RowStats& s, float& dsa, float& dsb) {
   const float xa = ok ? __builtin_fmaf(ra, ca, -s.lsa2) : kNegInf;
   const float pa = exp2_fast(xa);
-  if (WANT_B) {
+  if constexpr (WANT_B) {
     const float xb = ok ? __builtin_fmaf(rb, cb, -s.lsb2) : kNegInf;
     const float pb = exp2_fast(xb);
     dsb = s.g * (pb - pa);
   }
-  if (WANT_A) {
+  if constexpr (WANT_A) {
     const float u = __builtin_fmaf(ra, sa, -__builtin_fmaf(rb, sb, s.dl));
     dsa = (s.g * pa) * u;
+  }
+}
+
+// ----------------------------------------------------------------------------
+// One streamed tile of one wave, shared by both kernels. The wave owns 32
+// resident rows (queries for dQ, keys for dK) held as MFMA B operands ra_op,
+// rb_op; the stage holds 32 streamed rows of A and B. S = stage_rows x
+// resident^T, so in the result lane l owns resident row l % 32 and 16 streamed
+// rows. stats(i) returns the row statistics of element i and ok(i) whether
+// element i is an allowed pair. The gradient tiles accumulate
+//   grad[resident][d] += sum_streamed dS[streamed][resident] * X[streamed][d]
+// with X the streamed rows of the stage (transpose reads).
+// ----------------------------------------------------------------------------
+template <int DA, int DB, int MODE, bool MASK, typename StatsFn, typename OkFn>
+__device__ __forceinline__ void bwd_tile(const u32x4* stage, const bf16x8 (&ra_op)[DA / 16],
+                                         const bf16x8 (&rb_op)[DB / 16],
+                                         f32x16 (&ga)[(MODE & 2) ? DA / 32 : 1],
+                                         f32x16 (&gb)[(MODE & 1) ? DB / 32 : 1],
+                                         float ca, float cb, float sa, float sb, int lane,
+                                         StatsFn stats, OkFn ok) {
+  using C = BwdCfg<DA, DB, MODE>;
+  const int half = lane >> 5;
+  const u32x4* ta = stage;
+  const u32x4* tb = stage + C::BS * C::CA;
+  const int r = lane & 31;
+  f32x16 s_a = zero16(), s_b = zero16();
+#pragma unroll
+  for (int ks = 0; ks < DA / 16; ++ks) s_a = mfma32(lds_row8<C::CA>(ta, r, 2 * ks + half), ra_op[ks], s_a);
+#pragma unroll
+  for (int ks = 0; ks < DB / 16; ++ks) s_b = mfma32(lds_row8<C::CB>(tb, r, 2 * ks + half), rb_op[ks], s_b);
+  float dsa[16], dsb[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const RowStats rs = stats(i);
+    dlogits<C::WANT_A, C::WANT_B>(s_a[i], s_b[i], MASK ? ok(i) : true, ca, cb, sa, sb, rs, dsa[i], dsb[i]);
+  }
+  // transpose-read addressing (see kl_common.hpp): row 4 * half + (lane % 16) / 4 of each
+  // 16-row k-block, columns 16 * ((lane / 16) % 2) + 4 * (lane % 4) of each 32-column block.
+  const int tr_row = 4 * half + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    if constexpr (C::WANT_B) {
+      const bf16x8 aop = pack8(dsb + 8 * s);
+#pragma unroll
+      for (int nb = 0; nb < DB / 32; ++nb) {
+        const bf16x8 bop = cat8(lds_tr4<C::CB>(tb, 16 * s + tr_row, 32 * nb + tr_col),
+                                lds_tr4<C::CB>(tb, 16 * s + 8 + tr_row, 32 * nb + tr_col));
+        gb[nb] = mfma32(aop, bop, gb[nb]);
+      }
+    }
+    if constexpr (C::WANT_A) {
+      const bf16x8 aop = pack8(dsa + 8 * s);
+#pragma unroll
+      for (int nb = 0; nb < DA / 32; ++nb) {
+        const bf16x8 bop = cat8(lds_tr4<C::CA>(ta, 16 * s + tr_row, 32 * nb + tr_col),
+                                lds_tr4<C::CA>(ta, 16 * s + 8 + tr_row, 32 * nb + tr_col));
+        ga[nb] = mfma32(aop, bop, ga[nb]);
+      }
+    }
+  }
+}
+
+// Resident rows of this lane as MFMA B operands (zero rows past n).
+template <int D>
+__device__ __forceinline__ void load_resident(bf16x8 (&op)[D / 16], const uint16_t* X, size_t bh_rows, int row,
+                                              int n, int half) {
+  const bool ok = row < n;
+  const u32x4* p = reinterpret_cast<const u32x4*>(X + (bh_rows + (ok ? row : 0)) * D);
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks)
+    op[ks] = __builtin_bit_cast(bf16x8, ok ? p[2 * ks + half] : u32x4{0u, 0u, 0u, 0u});
+}
+
+// Write one gradient tile: lane l, register i holds row base + 8 (i / 4) + 4 half + i % 4,
+// column 32 nb + l % 32; the factor s of S = s Q K^T is applied here.
+template <int D>
+__device__ __forceinline__ void write_grad(float* out, const f32x16 (&acc)[D / 32], size_t bh_rows, int base,
+                                           int n, float s, int lane) {
+  const int half = lane >> 5;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int row = base + 8 * (i >> 2) + 4 * half + (i & 3);
+    if (row < n) {
+      float* o = out + (bh_rows + row) * D + (lane & 31);
+#pragma unroll
+      for (int nb = 0; nb < D / 32; ++nb) o[32 * nb] = acc[nb][i] * s;
+    }
   }
 }
 
@@ -96,7 +183,7 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
                  const float* __restrict__ lse_b, const float* __restrict__ g,
                  float* __restrict__ dQa, float* __restrict__ dQb) {
   using C = BwdCfg<DA, DB, MODE>;
-  __shared__ uint4 smem[2 * C::STAGE];
+  __shared__ u32x4 smem[2 * C::STAGE];   // two-stage ring of key tiles
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
   const int TQ = (NQ + C::BR - 1) / C::BR;
@@ -108,6 +195,7 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   const int off = NK - NQ;
   const int qw = q0 + 32 * wave;
   const int myq = qw + (lane & 31);
+  const int wlast = min(qw + 31, NQ - 1);
   const float ca = sa * kLog2e, cb = sb * kLog2e;
 
   int ntiles = (NK + C::BS - 1) / C::BS;
@@ -117,19 +205,9 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   }
 
   const RowStats rs = load_row_stats(kl, lse_a, lse_b, g, (size_t)bh * NQ + myq, myq < NQ);
-
   bf16x8 qa[DA / 16], qb[DB / 16];
-  {
-    const bool okq = myq < NQ;
-    const uint4* pa = reinterpret_cast<const uint4*>(Qa + ((size_t)bh * NQ + (okq ? myq : 0)) * DA);
-    const uint4* pb = reinterpret_cast<const uint4*>(Qb + ((size_t)bh * NQ + (okq ? myq : 0)) * DB);
-#pragma unroll
-    for (int ks = 0; ks < DA / 16; ++ks)
-      qa[ks] = __builtin_bit_cast(bf16x8, okq ? pa[2 * ks + half] : make_uint4(0, 0, 0, 0));
-#pragma unroll
-    for (int ks = 0; ks < DB / 16; ++ks)
-      qb[ks] = __builtin_bit_cast(bf16x8, okq ? pb[2 * ks + half] : make_uint4(0, 0, 0, 0));
-  }
+  load_resident<DA>(qa, Qa, (size_t)bh * NQ, myq, NQ, half);
+  load_resident<DB>(qb, Qb, (size_t)bh * NQ, myq, NQ, half);
 
   f32x16 dqa[C::WANT_A ? DA / 32 : 1], dqb[C::WANT_B ? DB / 32 : 1];
 #pragma unroll
@@ -137,54 +215,12 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
 #pragma unroll
   for (int n = 0; n < (C::WANT_B ? DB / 32 : 1); ++n) dqb[n] = zero16();
 
-  const uint4* gKa = reinterpret_cast<const uint4*>(Ka + (size_t)bh * NK * DA);
-  const uint4* gKb = reinterpret_cast<const uint4*>(Kb + (size_t)bh * NK * DB);
-  uint4 stg[C::CHT];
-  auto gload = [&](int kt) {
-    const int k0 = kt * C::BS;
-#pragma unroll
-    for (int i = 0; i < C::CHT; ++i) {
-      const int p = tid + kThreads * i;
-      if (i < C::CHT_A) {
-        const int r = p / C::CA, c = p - r * C::CA;
-        stg[i] = gKa[(size_t)min(k0 + r, NK - 1) * C::CA + c];
-      } else {
-        const int pp = p - C::BS * C::CA;
-        const int r = pp / C::CB, c = pp - r * C::CB;
-        stg[i] = gKb[(size_t)min(k0 + r, NK - 1) * C::CB + c];
-      }
-    }
-  };
-  auto lstore = [&](int buf) {
-    uint4* base = smem + buf * C::STAGE;
-#pragma unroll
-    for (int i = 0; i < C::CHT; ++i) {
-      const int p = tid + kThreads * i;
-      if (i < C::CHT_A) {
-        const int r = p / C::CA, c = p - r * C::CA;
-        base[chunk_slot<C::CA>(r, c)] = stg[i];
-      } else {
-        const int pp = p - C::BS * C::CA;
-        const int r = pp / C::CB, c = pp - r * C::CB;
-        base[C::BS * C::CA + chunk_slot<C::CB>(r, c)] = stg[i];
-      }
-    }
-  };
+  const rsrc_t rka = make_rsrc(Ka + (size_t)bh * NK * DA, (uint32_t)NK * DA * 2u);
+  const rsrc_t rkb = make_rsrc(Kb + (size_t)bh * NK * DB, (uint32_t)NK * DB * 2u);
+  const TileDma<C::BS, C::CA, C::CB> dma(tid);
+  const int kmax_ok = CAUSAL ? myq + off : NK;
 
-  const int wlast = min(qw + 31, NQ - 1);
-  // transpose-read addressing of this lane (see kl_common.hpp): row 4 * half + lane/4 % 4
-  // of each 16-row k-block, columns 16 * (lane/16 % 2) + 4 * (lane % 4) of each 32-column block.
-  const int tr_row = 4 * half + ((lane & 15) >> 2);
-  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-
-  if (ntiles > 0) {
-    gload(0);
-    lstore(0);
-  }
-  __syncthreads();
-  for (int kt = 0; kt < ntiles; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < ntiles) gload(kt + 1);
+  auto tile = [&](const u32x4* stage, int kt) {
     const int k0 = kt * C::BS;
     bool active = qw < NQ;
     bool need_mask = k0 + C::BS > NK;
@@ -192,66 +228,31 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
       active = active && (k0 <= wlast + off);
       need_mask = need_mask || (k0 + C::BS - 1 > qw + off);
     }
-    if (active) {
-      const uint4* ta = smem + buf * C::STAGE;
-      const uint4* tb = ta + C::BS * C::CA;
-      const int r = lane & 31;
-      f32x16 s_a = zero16(), s_b = zero16();
-#pragma unroll
-      for (int ks = 0; ks < DA / 16; ++ks) s_a = mfma32(lds_row8<C::CA>(ta, r, 2 * ks + half), qa[ks], s_a);
-#pragma unroll
-      for (int ks = 0; ks < DB / 16; ++ks) s_b = mfma32(lds_row8<C::CB>(tb, r, 2 * ks + half), qb[ks], s_b);
-      float dsa[16], dsb[16];
-      const int kmax_ok = CAUSAL ? myq + off : NK;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int k = k0 + 8 * (i >> 2) + 4 * half + (i & 3);
-        const bool ok = need_mask ? (k < NK && k <= kmax_ok) : true;
-        dlogits<C::WANT_A, C::WANT_B>(s_a[i], s_b[i], ok, ca, cb, sa, sb, rs, dsa[i], dsb[i]);
-      }
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        if (C::WANT_B) {
-          const bf16x8 aop = pack8(dsb + 8 * s);
-#pragma unroll
-          for (int nb = 0; nb < DB / 32; ++nb) {
-            const bf16x8 bop = cat8(lds_tr4<C::CB>(tb, 16 * s + tr_row, 32 * nb + tr_col),
-                                    lds_tr4<C::CB>(tb, 16 * s + 8 + tr_row, 32 * nb + tr_col));
-            dqb[nb] = mfma32(aop, bop, dqb[nb]);
-          }
-        }
-        if (C::WANT_A) {
-          const bf16x8 aop = pack8(dsa + 8 * s);
-#pragma unroll
-          for (int nb = 0; nb < DA / 32; ++nb) {
-            const bf16x8 bop = cat8(lds_tr4<C::CA>(ta, 16 * s + tr_row, 32 * nb + tr_col),
-                                    lds_tr4<C::CA>(ta, 16 * s + 8 + tr_row, 32 * nb + tr_col));
-            dqa[nb] = mfma32(aop, bop, dqa[nb]);
-          }
-        }
-      }
-    }
-    if (kt + 1 < ntiles) lstore(buf ^ 1);
+    if (!active) return;
+    auto stats = [&](int) { return rs; };
+    auto ok = [&](int i) {
+      const int k = k0 + 8 * (i >> 2) + 4 * half + (i & 3);
+      return k < NK && k <= kmax_ok;
+    };
+    if (need_mask)
+      bwd_tile<DA, DB, MODE, true>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, lane, stats, ok);
+    else
+      bwd_tile<DA, DB, MODE, false>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, lane, stats, ok);
+  };
+
+  if (ntiles > 0) dma.issue(rka, rkb, 0, smem, wave);
+  wait_vmem();
+  __syncthreads();
+  for (int kt = 0; kt < ntiles; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < ntiles) dma.issue(rka, rkb, (kt + 1) * C::BS, smem + (buf ^ 1) * C::STAGE, wave);
+    tile(smem + buf * C::STAGE, kt);
+    wait_vmem();
     __syncthreads();
   }
 
-  // Write: lane l, register i holds row qw + 8 (i / 4) + 4 half + i % 4, column 32 nb + l % 32.
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int q = qw + 8 * (i >> 2) + 4 * half + (i & 3);
-    if (q < NQ) {
-      if (C::WANT_B) {
-        float* out = dQb + ((size_t)bh * NQ + q) * DB + (lane & 31);
-#pragma unroll
-        for (int nb = 0; nb < DB / 32; ++nb) out[32 * nb] = dqb[nb][i] * sb;
-      }
-      if (C::WANT_A) {
-        float* out = dQa + ((size_t)bh * NQ + q) * DA + (lane & 31);
-#pragma unroll
-        for (int nb = 0; nb < DA / 32; ++nb) out[32 * nb] = dqa[nb][i] * sa;
-      }
-    }
-  }
+  if constexpr (C::WANT_B) write_grad<DB>(dQb, dqb, (size_t)bh * NQ, qw, NQ, sb, lane);
+  if constexpr (C::WANT_A) write_grad<DA>(dQa, dqa, (size_t)bh * NQ, qw, NQ, sa, lane);
 }
 
 // ----------------------------------------------------------------------------
@@ -267,18 +268,18 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
                  const float* __restrict__ lse_b, const float* __restrict__ g,
                  float* __restrict__ dKa, float* __restrict__ dKb) {
   using C = BwdCfg<DA, DB, MODE>;
-  __shared__ uint4 smem[2 * C::STAGE];
-  __shared__ f32x4 sstat[2][4][C::BS / 4];   // [stage][lsa2, lsb2, g, dl][4 rows]
+  __shared__ u32x4 smem[2 * C::STAGE];        // two-stage ring of query tiles
+  __shared__ f32x4 sstat[2][4][C::BS / 4];    // their row statistics: [stage][lsa2, lsb2, g, dl][rows / 4]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
   const int TK = (NK + C::BR - 1) / C::BR;
   const int logical = xcd_logical(blockIdx.x, gridDim.x);
   const int bh = logical / TK;
-  const int kt_blk = logical - bh * TK;     // causal: low key tiles see the most rows, so they go first
-  const int kb0 = kt_blk * C::BR;
+  const int kb0 = (logical - bh * TK) * C::BR;   // causal: low key blocks see the most rows, so they go first
   const int off = NK - NQ;
-  const int kw = kb0 + 32 * wave;           // first key of this wave
+  const int kw = kb0 + 32 * wave;
   const int myk = kw + (lane & 31);
+  const int wklast = min(kw + 31, NK - 1);
   const float ca = sa * kLog2e, cb = sb * kLog2e;
 
   const int ntq = (NQ + C::BS - 1) / C::BS;
@@ -288,19 +289,9 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
     t_begin = qmin <= 0 ? 0 : min(ntq, qmin / C::BS);
   }
 
-  // K rows of this lane as MFMA B operands.
   bf16x8 ka[DA / 16], kb[DB / 16];
-  {
-    const bool okk = myk < NK;
-    const uint4* pa = reinterpret_cast<const uint4*>(Ka + ((size_t)bh * NK + (okk ? myk : 0)) * DA);
-    const uint4* pb = reinterpret_cast<const uint4*>(Kb + ((size_t)bh * NK + (okk ? myk : 0)) * DB);
-#pragma unroll
-    for (int ks = 0; ks < DA / 16; ++ks)
-      ka[ks] = __builtin_bit_cast(bf16x8, okk ? pa[2 * ks + half] : make_uint4(0, 0, 0, 0));
-#pragma unroll
-    for (int ks = 0; ks < DB / 16; ++ks)
-      kb[ks] = __builtin_bit_cast(bf16x8, okk ? pb[2 * ks + half] : make_uint4(0, 0, 0, 0));
-  }
+  load_resident<DA>(ka, Ka, (size_t)bh * NK, myk, NK, half);
+  load_resident<DB>(kb, Kb, (size_t)bh * NK, myk, NK, half);
 
   f32x16 dka[C::WANT_A ? DA / 32 : 1], dkb[C::WANT_B ? DB / 32 : 1];
 #pragma unroll
@@ -308,64 +299,24 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
 #pragma unroll
   for (int n = 0; n < (C::WANT_B ? DB / 32 : 1); ++n) dkb[n] = zero16();
 
-  const uint4* gQa = reinterpret_cast<const uint4*>(Qa + (size_t)bh * NQ * DA);
-  const uint4* gQb = reinterpret_cast<const uint4*>(Qb + (size_t)bh * NQ * DB);
-  uint4 stg[C::CHT];
-  RowStats sst{0.f, 0.f, 0.f, 0.f};
-  auto gload = [&](int t) {
-    const int r0 = t * C::BS;
-#pragma unroll
-    for (int i = 0; i < C::CHT; ++i) {
-      const int p = tid + kThreads * i;
-      if (i < C::CHT_A) {
-        const int r = p / C::CA, c = p - r * C::CA;
-        stg[i] = gQa[(size_t)min(r0 + r, NQ - 1) * C::CA + c];
-      } else {
-        const int pp = p - C::BS * C::CA;
-        const int r = pp / C::CB, c = pp - r * C::CB;
-        stg[i] = gQb[(size_t)min(r0 + r, NQ - 1) * C::CB + c];
-      }
-    }
+  const rsrc_t rqa = make_rsrc(Qa + (size_t)bh * NQ * DA, (uint32_t)NQ * DA * 2u);
+  const rsrc_t rqb = make_rsrc(Qb + (size_t)bh * NQ * DB, (uint32_t)NQ * DB * 2u);
+  const TileDma<C::BS, C::CA, C::CB> dma(tid);
+
+  // Row statistics of a streamed tile: threads 0..31 each prepare one row.
+  auto stats_stage = [&](int t, f32x4 (&dst)[4][C::BS / 4]) {
     if (tid < C::BS) {
-      const int q = r0 + tid;
-      sst = load_row_stats(kl, lse_a, lse_b, g, (size_t)bh * NQ + q, q < NQ);
-    }
-  };
-  auto lstore = [&](int buf) {
-    uint4* base = smem + buf * C::STAGE;
-#pragma unroll
-    for (int i = 0; i < C::CHT; ++i) {
-      const int p = tid + kThreads * i;
-      if (i < C::CHT_A) {
-        const int r = p / C::CA, c = p - r * C::CA;
-        base[chunk_slot<C::CA>(r, c)] = stg[i];
-      } else {
-        const int pp = p - C::BS * C::CA;
-        const int r = pp / C::CB, c = pp - r * C::CB;
-        base[C::BS * C::CA + chunk_slot<C::CB>(r, c)] = stg[i];
-      }
-    }
-    if (tid < C::BS) {
-      float* s = reinterpret_cast<float*>(&sstat[buf][0][0]);
-      s[0 * C::BS + tid] = sst.lsa2;
-      s[1 * C::BS + tid] = sst.lsb2;
-      s[2 * C::BS + tid] = sst.g;
-      s[3 * C::BS + tid] = sst.dl;
+      const int q = t * C::BS + tid;
+      const RowStats s = load_row_stats(kl, lse_a, lse_b, g, (size_t)bh * NQ + q, q < NQ);
+      float* p = reinterpret_cast<float*>(&dst[0][0]);
+      p[0 * C::BS + tid] = s.lsa2;
+      p[1 * C::BS + tid] = s.lsb2;
+      p[2 * C::BS + tid] = s.g;
+      p[3 * C::BS + tid] = s.dl;
     }
   };
 
-  const int wklast = min(kw + 31, NK - 1);
-  const int tr_row = 4 * half + ((lane & 15) >> 2);
-  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-
-  if (t_begin < ntq) {
-    gload(t_begin);
-    lstore(0);
-  }
-  __syncthreads();
-  for (int t = t_begin; t < ntq; ++t) {
-    const int buf = (t - t_begin) & 1;
-    if (t + 1 < ntq) gload(t + 1);
+  auto tile = [&](const u32x4* stage, const f32x4 (&st)[4][C::BS / 4], int t) {
     const int r0 = t * C::BS;
     bool active = kw < NK;
     bool need_mask = r0 + C::BS > NQ;
@@ -374,76 +325,41 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
       active = active && (qlast + off >= kw);
       need_mask = need_mask || (wklast > r0 + off);
     }
-    if (active) {
-      const uint4* ta = smem + buf * C::STAGE;
-      const uint4* tb = ta + C::BS * C::CA;
-      const int r = lane & 31;
-      f32x16 s_a = zero16(), s_b = zero16();
-      // S[row][key]: A = Q rows from LDS, B = this wave's K rows.
-#pragma unroll
-      for (int ks = 0; ks < DA / 16; ++ks) s_a = mfma32(lds_row8<C::CA>(ta, r, 2 * ks + half), ka[ks], s_a);
-#pragma unroll
-      for (int ks = 0; ks < DB / 16; ++ks) s_b = mfma32(lds_row8<C::CB>(tb, r, 2 * ks + half), kb[ks], s_b);
-      float dsa[16], dsb[16];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        // rows 8 j + 4 half + 0..3 of the tile: one 16-byte read per statistic
-        const int rr = 8 * j + 4 * half;
-        const f32x4 vlsa = sstat[buf][0][rr / 4];
-        const f32x4 vlsb = sstat[buf][1][rr / 4];
-        const f32x4 vg = sstat[buf][2][rr / 4];
-        const f32x4 vdl = sstat[buf][3][rr / 4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int i = 4 * j + e;
-          const int q = r0 + rr + e;
-          const bool ok = need_mask ? (q < NQ && (!CAUSAL || myk <= q + off)) : true;
-          const RowStats rsq{vlsa[e], vlsb[e], vg[e], vdl[e]};
-          dlogits<C::WANT_A, C::WANT_B>(s_a[i], s_b[i], ok, ca, cb, sa, sb, rsq, dsa[i], dsb[i]);
-        }
-      }
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        if (C::WANT_B) {
-          const bf16x8 aop = pack8(dsb + 8 * s);
-#pragma unroll
-          for (int nb = 0; nb < DB / 32; ++nb) {
-            const bf16x8 bop = cat8(lds_tr4<C::CB>(tb, 16 * s + tr_row, 32 * nb + tr_col),
-                                    lds_tr4<C::CB>(tb, 16 * s + 8 + tr_row, 32 * nb + tr_col));
-            dkb[nb] = mfma32(aop, bop, dkb[nb]);
-          }
-        }
-        if (C::WANT_A) {
-          const bf16x8 aop = pack8(dsa + 8 * s);
-#pragma unroll
-          for (int nb = 0; nb < DA / 32; ++nb) {
-            const bf16x8 bop = cat8(lds_tr4<C::CA>(ta, 16 * s + tr_row, 32 * nb + tr_col),
-                                    lds_tr4<C::CA>(ta, 16 * s + 8 + tr_row, 32 * nb + tr_col));
-            dka[nb] = mfma32(aop, bop, dka[nb]);
-          }
-        }
-      }
+    if (!active) return;
+    // element i of this lane is streamed row r0 + 8 (i / 4) + 4 half + i % 4
+    auto stats = [&](int i) {
+      const int grp = 2 * (i >> 2) + half;
+      return RowStats{st[0][grp][i & 3], st[1][grp][i & 3], st[2][grp][i & 3], st[3][grp][i & 3]};
+    };
+    auto ok = [&](int i) {
+      const int q = r0 + 8 * (i >> 2) + 4 * half + (i & 3);
+      return q < NQ && (!CAUSAL || myk <= q + off);
+    };
+    if (need_mask)
+      bwd_tile<DA, DB, MODE, true>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, lane, stats, ok);
+    else
+      bwd_tile<DA, DB, MODE, false>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, lane, stats, ok);
+  };
+
+  if (t_begin < ntq) {
+    dma.issue(rqa, rqb, t_begin * C::BS, smem, wave);
+    stats_stage(t_begin, sstat[0]);
+  }
+  wait_vmem();
+  __syncthreads();
+  for (int t = t_begin; t < ntq; ++t) {
+    const int buf = (t - t_begin) & 1;
+    if (t + 1 < ntq) {
+      dma.issue(rqa, rqb, (t + 1) * C::BS, smem + (buf ^ 1) * C::STAGE, wave);
+      stats_stage(t + 1, sstat[buf ^ 1]);
     }
-    if (t + 1 < ntq) lstore(buf ^ 1);
+    tile(smem + buf * C::STAGE, sstat[buf], t);
+    wait_vmem();
     __syncthreads();
   }
 
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int k = kw + 8 * (i >> 2) + 4 * half + (i & 3);
-    if (k < NK) {
-      if (C::WANT_B) {
-        float* out = dKb + ((size_t)bh * NK + k) * DB + (lane & 31);
-#pragma unroll
-        for (int nb = 0; nb < DB / 32; ++nb) out[32 * nb] = dkb[nb][i] * sb;
-      }
-      if (C::WANT_A) {
-        float* out = dKa + ((size_t)bh * NK + k) * DA + (lane & 31);
-#pragma unroll
-        for (int nb = 0; nb < DA / 32; ++nb) out[32 * nb] = dka[nb][i] * sa;
-      }
-    }
-  }
+  if constexpr (C::WANT_B) write_grad<DB>(dKb, dkb, (size_t)bh * NK, kw, NK, sb, lane);
+  if constexpr (C::WANT_A) write_grad<DA>(dKa, dka, (size_t)bh * NK, kw, NK, sa, lane);
 }
 
 }  // namespace streamkl

@@ -21,6 +21,7 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));   // one 16-byte chunk
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(3))) char lds_char;
 
@@ -59,14 +60,14 @@ __device__ __forceinline__ int chunk_slot(int r, int c) { return r * CPR + (c ^ 
 
 // 8 consecutive bf16 (one chunk) of row r: an MFMA A/B operand.
 template <int CPR>
-__device__ __forceinline__ bf16x8 lds_row8(const uint4* tile, int r, int c) {
+__device__ __forceinline__ bf16x8 lds_row8(const u32x4* tile, int r, int c) {
   return __builtin_bit_cast(bf16x8, tile[chunk_slot<CPR>(r, c)]);
 }
 
 // Transpose read: the calling lane addresses 4 bf16 at (row r, column e),
 // e a multiple of 4; see the layout note at the top of this file.
 template <int CPR>
-__device__ __forceinline__ bf16x4 lds_tr4(const uint4* tile, int r, int e) {
+__device__ __forceinline__ bf16x4 lds_tr4(const u32x4* tile, int r, int e) {
   const int byte = chunk_slot<CPR>(r, e >> 3) * 16 + ((e >> 2) & 1) * 8;
   const lds_char* base = (const lds_char*)(tile);
   i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + byte));
@@ -87,6 +88,64 @@ __device__ __forceinline__ bf16x8 pack8(const float* v) {
   for (int t = 0; t < 8; ++t) r[t] = (__bf16)v[t];
   return r;
 }
+
+// ---------------------------------------------------------------------------
+// Tile staging by direct-to-LDS buffer loads (buffer_load_dwordx4 ... lds).
+// A buffer resource covers one [N, D] bf16 matrix of one (batch, head); reads
+// past its end return zeros, so ragged tails need no clamping (the kernels
+// mask those rows). One such load moves 64 x 16 bytes and writes them to LDS
+// at M0 + 16 * lane: wave w's i-th load fills chunk slots
+// 256 i + 64 w + lane of the stage, and each lane fetches whichever (row,
+// chunk) the swizzled layout stores in its slot. No VGPR holds tile data.
+// ---------------------------------------------------------------------------
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  // dword 3 = 0x00020000: raw (untyped) 32-bit data format, as used for gfx9 raw buffer access
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// s_waitcnt vmcnt(0) with expcnt and lgkmcnt left unconstrained (gfx9 encoding).
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+template <int R, int CA, int CB>
+struct TileDma {
+  static constexpr int NCH = R * (CA + CB) / kThreads;
+  static constexpr int NCH_A = R * CA / kThreads;
+  static_assert((R * (CA + CB)) % kThreads == 0 && (R * CA) % kThreads == 0, "staging split");
+  uint32_t voff[NCH];   // byte offset (from the tile's first row) of the chunk this lane fetches
+
+  __device__ __forceinline__ explicit TileDma(int tid) {
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      const int p = tid + kThreads * i;
+      if (i < NCH_A) {
+        const int r = p / CA, c = (p - r * CA) ^ swz(r);
+        voff[i] = (uint32_t)(r * CA + c) * 16u;
+      } else {
+        const int pp = p - R * CA;
+        const int r = pp / CB, c = (pp - r * CB) ^ swz(r);
+        voff[i] = (uint32_t)(r * CB + c) * 16u;
+      }
+    }
+  }
+
+  // Rows row0 .. row0 + R - 1 of A and B into `stage` (R * (CA + CB) chunks).
+  __device__ __forceinline__ void issue(rsrc_t ra, rsrc_t rb, int row0, u32x4* stage, int wave) const {
+#if defined(__HIP_DEVICE_COMPILE__)   // the host pass never runs this; keep its builtins out of it
+    const int soff_a = row0 * CA * 16, soff_b = row0 * CB * 16;
+#pragma unroll
+    for (int i = 0; i < NCH_A; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(stage + kThreads * i + 64 * wave), 16, voff[i],
+                                               soff_a, 0, 0);
+#pragma unroll
+    for (int i = NCH_A; i < NCH; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void*)(stage + kThreads * i + 64 * wave), 16, voff[i],
+                                               soff_b, 0, 0);
+#endif
+  }
+};
 
 // ---------------------------------------------------------------------------
 // Workgroup -> tile mapping. The dispatcher hands workgroup w to XCD w % 8,

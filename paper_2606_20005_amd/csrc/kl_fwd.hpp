@@ -34,11 +34,8 @@ struct FwdCfg {
   static constexpr int NMB = BK / 32;                       // 32-key MFMA blocks per tile
   static constexpr int CA = DA / 8, CB = DB / 8;            // 16-byte chunks per row
   static constexpr int STAGE = BK * (CA + CB);              // chunks per LDS stage
-  static constexpr int CHT = STAGE / kThreads;              // chunks each thread stages
-  static constexpr int CHT_A = BK * CA / kThreads;          // ... of which from K_a
   static constexpr int MINB = (DA + DB <= 256) ? 2 : 1;     // workgroups per CU to fit
   static_assert(DA % 64 == 0 && DB % 64 == 0, "head dims must be multiples of 64");
-  static_assert(STAGE % kThreads == 0 && (BK * CA) % kThreads == 0, "staging split");
 };
 
 // Five running row scalars of one half-wave (base-2 domain, see above).
@@ -107,6 +104,41 @@ __device__ __forceinline__ void fwd_tile_update(RowState& st, const f32x16 (&sa)
   st.mb = mb_new;
 }
 
+// One key tile of one wave: S^T tiles on the MFMA, then the online update.
+template <int DA, int DB, bool CAUSAL>
+__device__ __forceinline__ void fwd_tile(const u32x4* stage, const bf16x8 (&qa)[DA / 16], const bf16x8 (&qb)[DB / 16],
+                                         RowState& st, int k0, int NK, int qw, int wlast, int off, int myq,
+                                         float ca, float cb, int lane) {
+  using C = FwdCfg<DA, DB>;
+  bool active = qw <= wlast;
+  bool need_mask = k0 + C::BK > NK;
+  if (CAUSAL) {
+    active = active && (k0 <= wlast + off);
+    need_mask = need_mask || (k0 + C::BK - 1 > qw + off);
+  }
+  if (!active) return;
+  const int half = lane >> 5;
+  const u32x4* ta = stage;
+  const u32x4* tb = stage + C::BK * C::CA;
+  f32x16 sa[C::NMB], sb[C::NMB];
+#pragma unroll
+  for (int mb = 0; mb < C::NMB; ++mb) {
+    const int r = 32 * mb + (lane & 31);
+    f32x16 acc_a = zero16(), acc_b = zero16();
+#pragma unroll
+    for (int ks = 0; ks < DA / 16; ++ks) acc_a = mfma32(lds_row8<C::CA>(ta, r, 2 * ks + half), qa[ks], acc_a);
+#pragma unroll
+    for (int ks = 0; ks < DB / 16; ++ks) acc_b = mfma32(lds_row8<C::CB>(tb, r, 2 * ks + half), qb[ks], acc_b);
+    sa[mb] = acc_a;
+    sb[mb] = acc_b;
+  }
+  const int kbase = k0 + 4 * half;
+  if (need_mask)
+    fwd_tile_update<DA, DB, true>(st, sa, sb, ca, cb, kbase, NK, CAUSAL ? myq + off : NK);
+  else
+    fwd_tile_update<DA, DB, false>(st, sa, sb, ca, cb, kbase, NK, NK);
+}
+
 template <int DA, int DB, bool CAUSAL>
 __global__ void __launch_bounds__(kThreads, (FwdCfg<DA, DB>::MINB))
 kl_fwd_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
@@ -114,7 +146,8 @@ kl_fwd_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
               int NQ, int NK, float ca, float cb,
               float* __restrict__ kl, float* __restrict__ lse_a, float* __restrict__ lse_b) {
   using C = FwdCfg<DA, DB>;
-  __shared__ uint4 smem[2 * C::STAGE];
+  // two statically distinct stages: the tile being read and the one being filled
+  __shared__ u32x4 smem[2 * C::STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
   const int TQ = (NQ + C::BQ - 1) / C::BQ;
@@ -126,6 +159,7 @@ kl_fwd_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
   const int off = NK - NQ;        // bottom-right alignment: row i sees keys <= i + off
   const int qw = q0 + 32 * wave;  // first row of this wave
   const int myq = qw + (lane & 31);
+  const int wlast = min(qw + 31, NQ - 1);   // last valid row of this wave
 
   int ntiles = (NK + C::BK - 1) / C::BK;
   if (CAUSAL) {
@@ -137,92 +171,29 @@ kl_fwd_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
   bf16x8 qa[DA / 16], qb[DB / 16];
   {
     const bool okq = myq < NQ;
-    const uint4* pa = reinterpret_cast<const uint4*>(Qa + ((size_t)bh * NQ + (okq ? myq : 0)) * DA);
-    const uint4* pb = reinterpret_cast<const uint4*>(Qb + ((size_t)bh * NQ + (okq ? myq : 0)) * DB);
+    const u32x4* pa = reinterpret_cast<const u32x4*>(Qa + ((size_t)bh * NQ + (okq ? myq : 0)) * DA);
+    const u32x4* pb = reinterpret_cast<const u32x4*>(Qb + ((size_t)bh * NQ + (okq ? myq : 0)) * DB);
 #pragma unroll
     for (int ks = 0; ks < DA / 16; ++ks)
-      qa[ks] = __builtin_bit_cast(bf16x8, okq ? pa[2 * ks + half] : make_uint4(0, 0, 0, 0));
+      qa[ks] = __builtin_bit_cast(bf16x8, okq ? pa[2 * ks + half] : u32x4{0u, 0u, 0u, 0u});
 #pragma unroll
     for (int ks = 0; ks < DB / 16; ++ks)
-      qb[ks] = __builtin_bit_cast(bf16x8, okq ? pb[2 * ks + half] : make_uint4(0, 0, 0, 0));
+      qb[ks] = __builtin_bit_cast(bf16x8, okq ? pb[2 * ks + half] : u32x4{0u, 0u, 0u, 0u});
   }
 
-  const uint4* gKa = reinterpret_cast<const uint4*>(Ka + (size_t)bh * NK * DA);
-  const uint4* gKb = reinterpret_cast<const uint4*>(Kb + (size_t)bh * NK * DB);
-  uint4 stg[C::CHT];
-  // Stage key tile kt: thread tid moves chunks tid + 256 * i (rows past N_K
-  // repeat the last key row; their logits are masked).
-  auto gload = [&](int kt) {
-    const int k0 = kt * C::BK;
-#pragma unroll
-    for (int i = 0; i < C::CHT; ++i) {
-      const int p = tid + kThreads * i;
-      if (i < C::CHT_A) {
-        const int r = p / C::CA, c = p - r * C::CA;
-        stg[i] = gKa[(size_t)min(k0 + r, NK - 1) * C::CA + c];
-      } else {
-        const int pp = p - C::BK * C::CA;
-        const int r = pp / C::CB, c = pp - r * C::CB;
-        stg[i] = gKb[(size_t)min(k0 + r, NK - 1) * C::CB + c];
-      }
-    }
-  };
-  auto lstore = [&](int buf) {
-    uint4* base = smem + buf * C::STAGE;
-#pragma unroll
-    for (int i = 0; i < C::CHT; ++i) {
-      const int p = tid + kThreads * i;
-      if (i < C::CHT_A) {
-        const int r = p / C::CA, c = p - r * C::CA;
-        base[chunk_slot<C::CA>(r, c)] = stg[i];
-      } else {
-        const int pp = p - C::BK * C::CA;
-        const int r = pp / C::CB, c = pp - r * C::CB;
-        base[C::BK * C::CA + chunk_slot<C::CB>(r, c)] = stg[i];
-      }
-    }
-  };
-
+  const rsrc_t rka = make_rsrc(Ka + (size_t)bh * NK * DA, (uint32_t)NK * DA * 2u);
+  const rsrc_t rkb = make_rsrc(Kb + (size_t)bh * NK * DB, (uint32_t)NK * DB * 2u);
+  const TileDma<C::BK, C::CA, C::CB> dma(tid);
   RowState st{kNegInf, 0.f, kNegInf, 0.f, 0.f};
-  const int wlast = min(qw + 31, NQ - 1);   // last valid row of this wave
 
-  if (ntiles > 0) {
-    gload(0);
-    lstore(0);
-  }
+  if (ntiles > 0) dma.issue(rka, rkb, 0, smem, wave);
+  wait_vmem();
   __syncthreads();
   for (int kt = 0; kt < ntiles; ++kt) {
     const int buf = kt & 1;
-    if (kt + 1 < ntiles) gload(kt + 1);
-    const int k0 = kt * C::BK;
-    bool active = qw < NQ;
-    bool need_mask = k0 + C::BK > NK;
-    if (CAUSAL) {
-      active = active && (k0 <= wlast + off);
-      need_mask = need_mask || (k0 + C::BK - 1 > qw + off);
-    }
-    if (active) {
-      const uint4* ta = smem + buf * C::STAGE;
-      const uint4* tb = ta + C::BK * C::CA;
-      f32x16 sa[C::NMB], sb[C::NMB];
-#pragma unroll
-      for (int mb = 0; mb < C::NMB; ++mb) {
-        const int r = 32 * mb + (lane & 31);
-        f32x16 acc_a = zero16(), acc_b = zero16();
-#pragma unroll
-        for (int ks = 0; ks < DA / 16; ++ks) acc_a = mfma32(lds_row8<C::CA>(ta, r, 2 * ks + half), qa[ks], acc_a);
-#pragma unroll
-        for (int ks = 0; ks < DB / 16; ++ks) acc_b = mfma32(lds_row8<C::CB>(tb, r, 2 * ks + half), qb[ks], acc_b);
-        sa[mb] = acc_a;
-        sb[mb] = acc_b;
-      }
-      const int kbase = k0 + 4 * half;
-      if (need_mask)
-        fwd_tile_update<DA, DB, true>(st, sa, sb, ca, cb, kbase, NK, CAUSAL ? myq + off : NK);
-      else
-        fwd_tile_update<DA, DB, false>(st, sa, sb, ca, cb, kbase, NK, NK);
-    }
-    if (kt + 1 < ntiles) lstore(buf ^ 1);
+    if (kt + 1 < ntiles) dma.issue(rka, rkb, (kt + 1) * C::BK, smem + (buf ^ 1) * C::STAGE, wave);
+    fwd_tile<DA, DB, CAUSAL>(smem + buf * C::STAGE, qa, qb, st, kt * C::BK, NK, qw, wlast, off, myq, ca, cb, lane);
+    wait_vmem();
     __syncthreads();
   }
 
