@@ -28,6 +28,34 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_HBM_GBPS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+
+
+def kernel_source_hash():
+    """SHA-256 over the HIP sources and the C header: counters are only valid for the code they measured."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    files = sorted(glob.glob(os.path.join(ROOT, "paper_2606_20005_amd", "csrc", "*"))) + \
+        [os.path.join(ROOT, "include", "streamkl.h")]
+    for f in files:
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE passes,
+    scaled by the copy-kernel calibration; None if absent or taken on different kernel sources."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("csrc_sha256") != kernel_source_hash():
+        return None
+    k = t.get("kernels", {}).get(kernel)
+    return None if k is None else int(k["hbm_bytes"])
 
 
 def pairs(w, causal):
@@ -217,7 +245,8 @@ def main():
                    "event_step_ms": round(step_ms, 4)},
         "kernels": {k: kern[k] for k in ("fwd", "dq", "dk")},
         "roofline": {"kernel": names[dom], "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": measured_traffic(names[dom]),
                      "flop_per_launch": kern[dom]["flop_per_launch"], "avg_launch_ms": kern[dom]["ms"]},
         "extra_hbm": extra,
         "kl_mean": kl_mean,

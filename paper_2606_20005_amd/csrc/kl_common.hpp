@@ -29,7 +29,7 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.69314718055994531f;
 constexpr float kNegInf = -__builtin_inff();
 constexpr int kXcds = 8;        // MI355X: 8 accelerator complex dies, 32 CUs each
-constexpr int kThreads = 256;   // every kernel runs 4 waves of 64 lanes
+constexpr int kThreads = 256;   // threads of a 4-wave workgroup
 
 __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -48,15 +48,27 @@ __device__ __forceinline__ f32x16 zero16() {
 // ---------------------------------------------------------------------------
 // LDS tiles. A tile of R rows x D bf16 is stored as R * (D / 8) 16-byte
 // chunks, row after row, with chunk c of row r placed at slot c ^ swz(r).
-// The XOR permutes the low three chunk bits so that
-//  - eight consecutive rows read at the same chunk (MFMA operand rows) and
-//  - four consecutive rows read at two adjacent chunks (transpose reads)
-// fall on distinct 16-byte bank groups. Needs D a multiple of 64.
+// The gfx950 LDS serves a 16-byte-per-lane read 16 lanes at a time from 64
+// four-byte banks, i.e. 16 chunk slots; a 16-lane group must touch 16
+// distinct slots modulo 16. The two read patterns are
+//  - MFMA operand rows: 16 consecutive rows at the same chunk, and
+//  - transpose reads: 4 consecutive rows (first one a multiple of 4) at
+//    4 consecutive chunks (first one a multiple of 4), two 16-lane groups.
+// For rows of 16 or 32 chunks (D = 128, 256) slot mod 16 is the chunk's low
+// four bits: XOR them with 4 (r mod 4) + (r / 4 mod 4), a bijection over 16
+// rows that moves 4 consecutive rows to 4 disjoint aligned chunk quads. For
+// rows of 8 or 24 chunks (D = 64, 192) two rows share the 16 slots: XOR the
+// low three bits with 4 (r / 2 mod 2) + (r / 4 mod 4), which separates rows
+// of equal parity the same way.
 // ---------------------------------------------------------------------------
-__host__ __device__ constexpr int swz(int r) { return ((r & 3) << 1) | ((r >> 2) & 1); }
+template <int CPR>
+__host__ __device__ constexpr int swz(int r) {
+  static_assert(CPR % 8 == 0, "rows must be a multiple of 8 chunks (D a multiple of 64)");
+  return (CPR % 16 == 0) ? (4 * (r & 3) + ((r >> 2) & 3)) : (4 * ((r >> 1) & 1) + ((r >> 2) & 3));
+}
 
 template <int CPR>
-__device__ __forceinline__ int chunk_slot(int r, int c) { return r * CPR + (c ^ swz(r)); }
+__device__ __forceinline__ int chunk_slot(int r, int c) { return r * CPR + (c ^ swz<CPR>(r)); }
 
 // 8 consecutive bf16 (one chunk) of row r: an MFMA A/B operand.
 template <int CPR>
@@ -106,43 +118,51 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
-// s_waitcnt vmcnt(0) with expcnt and lgkmcnt left unconstrained (gfx9 encoding).
-__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// s_waitcnt vmcnt(N) with expcnt and lgkmcnt left unconstrained (gfx9
+// encoding: vmcnt bits [3:0] and [15:14], expcnt [6:4], lgkmcnt [11:8]).
+template <int N>
+__device__ __forceinline__ void wait_vmem_le() {
+  static_assert(N >= 0 && N < 64, "vmcnt is a 6-bit counter");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+__device__ __forceinline__ void wait_vmem() { wait_vmem_le<0>(); }
 
-template <int R, int CA, int CB>
+template <int R, int CA, int CB, int NT = kThreads>
 struct TileDma {
-  static constexpr int NCH = R * (CA + CB) / kThreads;
-  static constexpr int NCH_A = R * CA / kThreads;
-  static_assert((R * (CA + CB)) % kThreads == 0 && (R * CA) % kThreads == 0, "staging split");
+  static constexpr int NCH = R * (CA + CB) / NT;
+  static constexpr int NCH_A = R * CA / NT;
+  static_assert((R * (CA + CB)) % NT == 0 && (R * CA) % NT == 0, "staging split");
   uint32_t voff[NCH];   // byte offset (from the tile's first row) of the chunk this lane fetches
 
   __device__ __forceinline__ explicit TileDma(int tid) {
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
-      const int p = tid + kThreads * i;
+      const int p = tid + NT * i;
       if (i < NCH_A) {
-        const int r = p / CA, c = (p - r * CA) ^ swz(r);
+        const int r = p / CA, c = (p - r * CA) ^ swz<CA>(r);
         voff[i] = (uint32_t)(r * CA + c) * 16u;
       } else {
         const int pp = p - R * CA;
-        const int r = pp / CB, c = (pp - r * CB) ^ swz(r);
+        const int r = pp / CB, c = (pp - r * CB) ^ swz<CB>(r);
         voff[i] = (uint32_t)(r * CB + c) * 16u;
       }
     }
   }
 
   // Rows row0 .. row0 + R - 1 of A and B into `stage` (R * (CA + CB) chunks).
+  // The row offset goes into the per-lane offset, which the buffer range
+  // check covers (the scalar offset is not range checked).
   __device__ __forceinline__ void issue(rsrc_t ra, rsrc_t rb, int row0, u32x4* stage, int wave) const {
 #if defined(__HIP_DEVICE_COMPILE__)   // the host pass never runs this; keep its builtins out of it
-    const int soff_a = row0 * CA * 16, soff_b = row0 * CB * 16;
+    const uint32_t base_a = (uint32_t)row0 * CA * 16u, base_b = (uint32_t)row0 * CB * 16u;
 #pragma unroll
     for (int i = 0; i < NCH_A; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(stage + kThreads * i + 64 * wave), 16, voff[i],
-                                               soff_a, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(stage + NT * i + 64 * wave), 16,
+                                               voff[i] + base_a, 0, 0, 0);
 #pragma unroll
     for (int i = NCH_A; i < NCH; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void*)(stage + kThreads * i + 64 * wave), 16, voff[i],
-                                               soff_b, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void*)(stage + NT * i + 64 * wave), 16,
+                                               voff[i] + base_b, 0, 0, 0);
 #endif
   }
 };

@@ -9,7 +9,7 @@ static hipError_t run_fwd(const FwdArgs& a) {
   using C = FwdCfg<DA, DB>;
   const int tq = (a.NQ + C::BQ - 1) / C::BQ;
   const dim3 grid((unsigned)((long long)a.BH * tq));
-  hipLaunchKernelGGL((kl_fwd_kernel<DA, DB, CAUSAL>), grid, dim3(kThreads), 0, a.stream,
+  hipLaunchKernelGGL((kl_fwd_kernel<C, CAUSAL>), grid, dim3(kThreads), 0, a.stream,
                      a.Qa, a.Ka, a.Qb, a.Kb, a.NQ, a.NK, a.ca, a.cb, a.kl, a.lse_a, a.lse_b);
   return hipGetLastError();
 }
