@@ -198,21 +198,31 @@ def head_stats_all_rows(Q1, K1, Q2, K2, s1, s2, causal, direction, b, h, row_blo
 def dk_rows(Q1, K1, Q2, K2, s1, s2, causal, direction, b, h, keys, g, row_block=256):
     """dK1[keys], dK2[keys] of head (b, h): dK_t = s_t dS_t^T q_t summed over all rows.
 
-    g: [N_Q] upstream gradient of this head. The LSE and KL of every row are
-    computed first (a full forward of the head); then only the columns
-    ``keys`` of dS are formed, row block by row block.
+    g: [N_Q] upstream gradient of this head. The LSE and KL of every row that
+    can attend at least one of ``keys`` are computed first (a forward of those
+    rows); then only the columns ``keys`` of dS are formed, row block by row
+    block. Under the causal mask a row i sees key j only when
+    j <= N_K - N_Q + i, so rows before min(keys) - (N_K - N_Q) have every
+    sampled column masked: their terms are exactly zero and are not formed.
     """
     _check_direction(direction)
     s1, s2 = _f32(s1), _f32(s2)
     keys = np.asarray(keys, dtype=np.int64).reshape(-1)
     n_q, n_k = Q1.shape[2], K1.shape[2]
-    kl, lse1, lse2 = head_stats_all_rows(Q1, K1, Q2, K2, s1, s2, causal, direction, b, h, row_block)
+    r_first = max(0, int(keys.min()) - (n_k - n_q)) if causal else 0
+    kl = np.zeros(n_q)
+    lse1 = np.full(n_q, -np.inf)
+    lse2 = np.full(n_q, -np.inf)
+    for r0 in range(r_first, n_q, row_block):
+        rows = np.arange(r0, min(n_q, r0 + row_block))
+        kl[rows], lse1[rows], lse2[rows] = forward_rows(
+            Q1, K1, Q2, K2, s1, s2, causal, direction, b, h, rows)
     q1h, q2h = _head(Q1, b, h), _head(Q2, b, h)
     k1c, k2c = _head(K1, b, h)[keys], _head(K2, b, h)[keys]
     g = np.asarray(g, dtype=np.float64).reshape(-1)
     dk1 = np.zeros((keys.size, q1h.shape[1]))
     dk2 = np.zeros((keys.size, q2h.shape[1]))
-    for r0 in range(0, n_q, row_block):
+    for r0 in range(r_first, n_q, row_block):
         rows = np.arange(r0, min(n_q, r0 + row_block))
         mask = allowed_mask(rows, n_q, n_k, causal)[:, keys]
         S1 = s1 * (q1h[rows] @ k1c.T)

@@ -1,0 +1,128 @@
+"""GPU parity at the full workload sizes, in the configuration the benchmark
+launches (student gradients dQ2, dK2 of KL(P1 || P2)).
+
+The oracle cannot evaluate a whole 16K-128K head in seconds, so each workload
+is checked on sampled outputs that it computes one by one:
+  * KL, LSE1, LSE2 and dQ2 of sampled query rows (first, last, tile edges and
+    random rows) of three heads;
+  * dK2 of sampled keys of one head (random keys where the oracle can afford
+    the head's full statistics, else the last keys, which under the causal
+    mask only the last rows attend);
+and on properties that hold at any size, over every row and head:
+  * KL >= 0 (Gibbs) within the row tolerance, LSE finite;
+  * sum_j dK2[j] = 0 (each row of dS sums to zero);
+  * <dQ2, Q2> = <dK2, K2> per head (both equal sum_ij dS_ij S_ij).
+The property tolerances are relative to the magnitude of the summed terms: dS
+is rounded to bf16 before the second product, which breaks the exact zero
+row sums by at most 2^-9 per term.
+"""
+import time
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_20005_amd import inputs
+from parity_utils import GRAD_REL_L2, KL_ATOL, check_grad, check_rows, to_gpu_f32, upload
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+PROPERTY_REL = 1e-2
+
+
+def _sample_rows(n_q, rng, k=48):
+    fixed = [0, 1, 31, 32, 127, 128, n_q // 2, n_q - 129, n_q - 128, n_q - 2, n_q - 1]
+    extra = rng.choice(n_q, size=k, replace=False)
+    return np.unique(np.clip(np.concatenate([fixed, extra]), 0, n_q - 1))
+
+
+def _sample_keys(w, causal, rng, full_stats_ok, k=24):
+    if full_stats_ok or not causal:
+        fixed = [0, 1, 127, 128, w.n_k // 2, w.n_k - 1]
+        extra = rng.choice(w.n_k, size=k, replace=False)
+    else:
+        lo = w.n_k - 1024   # rows attending these keys: the last 1024 + (N_Q - N_K) ones
+        fixed = [lo, lo + 127, lo + 128, w.n_k - 129, w.n_k - 128, w.n_k - 1]
+        extra = lo + rng.choice(1024, size=k, replace=False)
+    return np.unique(np.concatenate([fixed, extra]))
+
+
+def _log(msg):
+    print(msg, flush=True)
+
+
+def _run_full(sk, name, causal, full_stats_ok):
+    import torch
+    t0 = time.time()
+    d = inputs.make(name)
+    w = d["w"]
+    _log(f"[fullsize] {name} causal={causal} B={w.B} H={w.H} NQ={w.n_q} NK={w.n_k} d1={w.d1} d2={w.d2}")
+    q1, k1, q2, k2 = upload(d)
+    g = to_gpu_f32(d["g"])
+    kl, l1, l2 = sk.fwd(q1, k1, q2, k2, w.s1, w.s2, causal, 0)
+    _, _, dq2, dk2 = sk.bwd(q1, k1, q2, k2, kl, l1, l2, g, w.s1, w.s2, causal, 0, want=("dq2", "dk2"))
+    torch.cuda.synchronize()
+    _log(f"[fullsize] {name}: inputs + GPU pass {time.time() - t0:.1f} s")
+
+    # --- properties over every row and head
+    assert bool(torch.isfinite(kl).all()) and bool(torch.isfinite(l1).all()) and bool(torch.isfinite(l2).all())
+    assert float(kl.min()) >= -KL_ATOL, f"KL below zero: {float(kl.min())}"
+    assert bool(torch.isfinite(dq2).all()) and bool(torch.isfinite(dk2).all())
+    dq = dq2.double()
+    dk = dk2.double()
+    q2d = q2.double()
+    k2d = k2.double()
+    col_sum = dk.sum(dim=2)                                     # [B, H, d2]
+    dk_norm = dk.pow(2).sum(dim=(2, 3)).sqrt()                  # [B, H]
+    ratio = (col_sum.pow(2).sum(dim=2).sqrt() / dk_norm).max().item()
+    _log(f"[fullsize] {name}: max_h ||sum_j dK2[j]|| / ||dK2||_F = {ratio:.2e}")
+    assert ratio <= PROPERTY_REL
+    a = (dq * q2d).sum(dim=(2, 3))
+    b = (dk * k2d).sum(dim=(2, 3))
+    scale = (dq * q2d).sum(dim=3).abs().sum(dim=2)
+    rel = ((a - b).abs() / scale).max().item()
+    _log(f"[fullsize] {name}: max_h |<dQ2,Q2> - <dK2,K2>| / sum_i |dQ2_i . Q2_i| = {rel:.2e}")
+    assert rel <= PROPERTY_REL
+    del dq, dk, q2d, k2d
+
+    # --- sampled rows of three heads against the oracle
+    rng = np.random.default_rng(w.seed)
+    heads = sorted({(0, 0), (w.B - 1, w.H - 1), (int(rng.integers(w.B)), int(rng.integers(w.H)))})
+    args = (d["Q1"], d["K1"], d["Q2"], d["K2"], w.s1, w.s2, causal, 0)
+    for b_, h_ in heads:
+        rows = _sample_rows(w.n_q, rng)
+        rk, r1, r2 = oracle.forward_rows(*args, b_, h_, rows)
+        ridx = torch.as_tensor(rows, device=kl.device)
+        check_rows("kl", kl[b_, h_, ridx].cpu().numpy(), rk)
+        check_rows("lse1", l1[b_, h_, ridx].cpu().numpy(), r1)
+        check_rows("lse2", l2[b_, h_, ridx].cpu().numpy(), r2)
+        _, rq2 = oracle.dq_rows(*args, b_, h_, rows, d["g"][b_, h_, rows])
+        e = check_grad("dq2", dq2[b_, h_, ridx].cpu().numpy(), rq2)
+        _log(f"[fullsize] {name}: head ({b_},{h_}) {rows.size} rows ok, dQ2 rel L2 {e:.2e}")
+
+    # --- sampled keys of one head
+    b_, h_ = heads[-1]
+    keys = _sample_keys(w, causal, rng, full_stats_ok)
+    t1 = time.time()
+    _, rk2 = oracle.dk_rows(*args, b_, h_, keys, d["g"][b_, h_], row_block=512)
+    kidx = torch.as_tensor(keys, device=kl.device)
+    e = check_grad("dk2", dk2[b_, h_, kidx].cpu().numpy(), rk2)
+    assert e <= GRAD_REL_L2
+    _log(f"[fullsize] {name}: head ({b_},{h_}) {keys.size} keys ok, dK2 rel L2 {e:.2e} "
+         f"(oracle {time.time() - t1:.1f} s); total {time.time() - t0:.1f} s")
+
+
+def test_fullsize_distill_causal(gpu_lib):
+    _run_full(gpu_lib, "distill", True, full_stats_ok=True)
+
+
+def test_fullsize_mid_noncausal(gpu_lib):
+    _run_full(gpu_lib, "mid", False, full_stats_ok=True)
+
+
+def test_fullsize_long_causal(gpu_lib):
+    _run_full(gpu_lib, "long", True, full_stats_ok=False)
+
+
+def test_fullsize_indexer_causal(gpu_lib):
+    _run_full(gpu_lib, "indexer", True, full_stats_ok=False)

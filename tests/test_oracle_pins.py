@@ -293,6 +293,24 @@ def test_dq_dk_rows_match_full_backward():
             a, b = oracle.dk_rows(Q1, K1, Q2, K2, 0.7, 0.3, causal, direction, 0, 1, keys, g[0, 1], row_block=6)
             np.testing.assert_allclose(a, dK1[0, 1, keys], rtol=1e-12, atol=1e-14)
             np.testing.assert_allclose(b, dK2[0, 1, keys], rtol=1e-12, atol=1e-14)
+            # tail keys: under the causal mask only the last rows are formed
+            tail = np.array([17, 21, 23])
+            a, b = oracle.dk_rows(Q1, K1, Q2, K2, 0.7, 0.3, causal, direction, 0, 1, tail, g[0, 1], row_block=6)
+            np.testing.assert_allclose(a, dK1[0, 1, tail], rtol=1e-12, atol=1e-14)
+            np.testing.assert_allclose(b, dK2[0, 1, tail], rtol=1e-12, atol=1e-14)
+
+
+@pytest.mark.parametrize("n_q,n_k", [(24, 10), (10, 24)])
+def test_dk_rows_tail_keys_unequal_lengths(n_q, n_k):
+    """Sampled dK of tail keys (rows skipped by the causal mask) equals the full
+    backward, with more queries than keys (empty rows) and fewer."""
+    Q1, K1, Q2, K2 = _rand_case(B=1, H=1, n_q=n_q, n_k=n_k, d1=4, d2=6, seed=18)
+    g = np.random.default_rng(19).uniform(0.5, 1.5, (1, 1, n_q))
+    _, _, _, _, dK1, _, dK2 = oracle.backward(Q1, K1, Q2, K2, 0.5, 0.9, True, FWD, g, row_block=5)
+    for keys in (np.array([n_k - 1]), np.array([n_k - 3, n_k - 2]), np.arange(n_k)):
+        a, b = oracle.dk_rows(Q1, K1, Q2, K2, 0.5, 0.9, True, FWD, 0, 0, keys, g[0, 0], row_block=4)
+        np.testing.assert_allclose(a, dK1[0, 0, keys], rtol=1e-12, atol=1e-14)
+        np.testing.assert_allclose(b, dK2[0, 0, keys], rtol=1e-12, atol=1e-14)
 
 
 def test_scale_invariance_identity_of_gradients():
