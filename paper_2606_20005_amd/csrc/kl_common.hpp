@@ -127,6 +127,24 @@ __device__ __forceinline__ void wait_vmem_le() {
 }
 __device__ __forceinline__ void wait_vmem() { wait_vmem_le<0>(); }
 
+// Workgroup barrier without a memory fence. __syncthreads() also releases and
+// acquires memory, which on gfx950 waits for every outstanding vector memory
+// operation of the wave, the tile loads still streaming into LDS included,
+// and so would drain the load pipeline at every barrier. The ring protocols
+// here do not need that: before a barrier that publishes a stage, the waves
+// that loaded it wait for exactly those loads (wait_vmem_le), and every LDS
+// read of a stage has returned before the barrier that lets it be refilled
+// (its value has been consumed). The signal fences keep the compiler from
+// moving memory accesses across the barrier, the scheduling barriers keep it
+// from moving any instruction across (phases stay where the code puts them).
+__device__ __forceinline__ void barrier_no_fence() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 template <int R, int CA, int CB, int NT = kThreads>
 struct TileDma {
   static constexpr int NCH = R * (CA + CB) / NT;

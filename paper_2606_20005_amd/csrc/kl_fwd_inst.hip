@@ -1,4 +1,4 @@
-// Instantiations and launcher of the forward kernel for every head-dim pair.
+// Instantiations and launcher of the forward kernels for every head-dim pair.
 #include "kl_fwd.hpp"
 #include "kl_launch.hpp"
 
@@ -9,7 +9,7 @@ static hipError_t run_fwd(const FwdArgs& a) {
   using C = FwdCfg<DA, DB>;
   const int tq = (a.NQ + C::BQ - 1) / C::BQ;
   const dim3 grid((unsigned)((long long)a.BH * tq));
-  hipLaunchKernelGGL((kl_fwd_kernel<C, CAUSAL>), grid, dim3(kThreads), 0, a.stream,
+  hipLaunchKernelGGL((kl_fwd_kernel<C, CAUSAL>), grid, dim3(C::NT), 0, a.stream,
                      a.Qa, a.Ka, a.Qb, a.Kb, a.NQ, a.NK, a.ca, a.cb, a.kl, a.lse_a, a.lse_b);
   return hipGetLastError();
 }
