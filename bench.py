@@ -10,9 +10,11 @@ then dK2 via the key-owned kernel) with the paper's mean objective
 Workload (the one the 16K figure is quoted on): B=1, H=32, N_Q=N_K=16384,
 d1=d2=128, s=1/sqrt(128), non-causal, student Q2 = bf16(Q1 + 0.3 eps), K2 = K1.
 Prints ONE JSON line. The 64K causal long-context figures (d1=128, d2=64,
-outlier channels) ride along in "long_context" unless --no-64k.
+outlier channels) ride along in "long_context" unless --no-64k, and the
+split-K forward on decode-like shapes (16 heads of 1-64 query rows over 64K
+keys) in "split_k" unless --no-split.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-64k] [--no-cpu-baseline]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-64k] [--no-cpu-baseline] [--no-split]
 """
 from __future__ import annotations
 
@@ -146,6 +148,43 @@ def run_workload(sk, w, causal, steps, warmup):
     return ms, wall_ms, extra, kl_mean
 
 
+def split_k_figures(sk, reps=10):
+    """Split-K forward (Sec. 3.3) against the single pass on decode-like shapes:
+    16 heads of N_Q in {1, 16, 64} rows over N_K = 65536 keys, d1 = d2 = 128,
+    non-causal (the shape family of the paper's split-K ablation). Inputs are
+    seeded N(0,1) drawn on the device; HIP events over `reps` launches each."""
+    import torch
+    B, H, NK, D = 16, 1, 65536, 128
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(2606200050 + 6)
+    k1 = torch.randn((B, H, NK, D), generator=gen, device="cuda").to(torch.bfloat16)
+    k2 = torch.randn((B, H, NK, D), generator=gen, device="cuda").to(torch.bfloat16)
+    s = D ** -0.5
+    out = []
+    for nq in (1, 16, 64):
+        q1 = torch.randn((B, H, nq, D), generator=gen, device="cuda").to(torch.bfloat16)
+        q2 = torch.randn((B, H, nq, D), generator=gen, device="cuda").to(torch.bfloat16)
+        res = {"n_q": nq}
+        for label, fn in (("single_pass", lambda: sk.fwd(q1, k1, q2, k2, s, s, False, 0)),
+                          ("split", lambda: sk.fwd_split(q1, k1, q2, k2, s, s, False, 0, splits="auto"))):
+            fn()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            res[label + "_ms"] = round(e0.elapsed_time(e1) / reps, 4)
+        res["splits"] = sk.split_count(B, H, nq, NK, D, D)
+        res["speedup"] = round(res["single_pass_ms"] / res["split_ms"], 2)
+        res["split_tflops"] = round(2 * 2 * D * B * H * nq * NK / (res["split_ms"] * 1e-3) / 1e12, 2)
+        out.append(res)
+    del k1, k2
+    torch.cuda.empty_cache()
+    return {"workload": f"B={B} H={H} N_K={NK} d1=d2={D} non-causal, N_Q in (1, 16, 64)", "rows": out}
+
+
 def summarize(w, causal, ms):
     P = pairs(w, causal)
     f = flops_per_pair(w)
@@ -197,6 +236,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-64k", action="store_true", help="skip the 64K long-context figures")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-split", action="store_true", help="skip the split-K decode-shape figures")
     ap.add_argument("--causal", action="store_true", help="run the 16K workload with causal masking")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run one 1 GiB device copy (reference kernel for HBM counters)")
@@ -261,6 +301,8 @@ def main():
             "fwd_frac_bf16_peak": kern_l["fwd"]["frac_bf16_peak"], "bwd_ms": kern_l["bwd"]["ms"],
             "bwd_tflops_algorithmic": kern_l["bwd"]["tflops_algorithmic"], "extra_hbm": extra_l,
             "naive_p1_p2_bytes": 2 * 2 * P_l, "kl_mean": kl_l}
+    if not a.no_split:
+        res["split_k"] = split_k_figures(sk)
     if a.copy_calibration:
         x = torch.empty(1 << 28, dtype=torch.float32, device="cuda")   # 1 GiB
         y = torch.empty_like(x)

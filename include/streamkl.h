@@ -104,6 +104,45 @@ int streamkl_bwd(const void* Q1, const void* K1, const void* Q2, const void* K2,
                  float* dQ1, float* dK1, float* dQ2, float* dK2,
                  hipStream_t stream);
 
+/*
+ * Split-K forward (Sec. 3.3, "Split-K variant" and "Adaptive split
+ * selection"): for heads with few query rows, the key range is cut into
+ * `splits` contiguous chunks of whole 32-key tiles, each (head, query block,
+ * chunk) runs the online pass of streamkl_fwd over its chunk and stores the
+ * five row statistics (m1, l1, m2, l2, acc) in `workspace`, and a reduce
+ * kernel merges the chunks per row with the rescaling rule of Sec. 3.3
+ * (associative, so the result equals streamkl_fwd up to fp32 rounding).
+ * Arguments and outputs are those of streamkl_fwd, plus:
+ *   splits          >= 1; 1 runs streamkl_fwd itself and needs no workspace.
+ *                   streamkl_fwd_split_count gives the paper's adaptive choice.
+ *   workspace       device memory owned by the caller, 4-byte aligned, at
+ *                   least streamkl_fwd_split_workspace_bytes(B, H, N_Q, splits)
+ *                   bytes; its contents on entry are ignored and on return
+ *                   are unspecified. Two calls may share it only if they are
+ *                   ordered on one stream.
+ *   workspace_bytes its size in bytes (smaller than required:
+ *                   STREAMKL_ERR_INVALID_ARG, nothing launched).
+ */
+int streamkl_fwd_split(const void* Q1, const void* K1, const void* Q2, const void* K2,
+                       int B, int H, int N_Q, int N_K, int d1, int d2,
+                       float s1, float s2, int causal, int direction, int splits,
+                       void* workspace, size_t workspace_bytes,
+                       float* kl, float* lse1, float* lse2,
+                       hipStream_t stream);
+
+/* Workspace bytes streamkl_fwd_split needs: 20 * splits * B * H * N_Q when
+   splits > 1, else 0. Returns 0 for negative extents. */
+size_t streamkl_fwd_split_workspace_bytes(int B, int H, int N_Q, int splits);
+
+/*
+ * Adaptive split count (Sec. 3.3): with P_base the number of workgroups the
+ * single-pass forward launches for these shapes and P_target = 512 (two per
+ * CU of an MI355X), returns 1 when P_base >= P_target and otherwise
+ * min(floor(P_target / P_base), number of 32-key tiles), at least 1.
+ * Returns 0 for invalid or unsupported arguments.
+ */
+int streamkl_fwd_split_count(int B, int H, int N_Q, int N_K, int d1, int d2);
+
 /* Static description of a status code. Never NULL. */
 const char* streamkl_strerror(int status);
 

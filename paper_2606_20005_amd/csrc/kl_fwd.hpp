@@ -182,37 +182,50 @@ __device__ __forceinline__ void load_q_operands(bf16x8 (&q)[D / 16], const uint1
     q[ks] = __builtin_bit_cast(bf16x8, okq ? p[2 * ks + half] : u32x4{0u, 0u, 0u, 0u});
 }
 
-// Merge the two half-waves of each row (split-K merge of Sec. 3.3) and write
-// KL (eq:kl-final), LSE_a and LSE_b (natural log) of the lane's row.
-__device__ __forceinline__ void fwd_finish(const RowState& st, float ca, float cb, int half, bool write, size_t ri,
-                                           float* __restrict__ kl, float* __restrict__ lse_a,
-                                           float* __restrict__ lse_b) {
-  RowState o;
-  o.mra = __shfl_xor(st.mra, 32);
-  o.la = __shfl_xor(st.la, 32);
-  o.mrb = __shfl_xor(st.mrb, 32);
-  o.lb = __shfl_xor(st.lb, 32);
-  o.acc = __shfl_xor(st.acc, 32);
-  if (half == 0 && write) {
-    auto scaled = [](float c, float m) { return m < kNoKeyRaw ? kNegInf : c * m; };
-    const float m0a = scaled(ca, st.mra), m1a = scaled(ca, o.mra);
-    const float m0b = scaled(cb, st.mrb), m1b = scaled(cb, o.mrb);
-    const float ma = fmaxf(m0a, m1a), mb = fmaxf(m0b, m1b);
-    float out_kl = 0.f, out_la = kNegInf, out_lb = kNegInf;
-    if (ma != kNegInf) {
-      const float f0 = exp2_fast(m0a - ma), f1 = exp2_fast(m1a - ma);
-      const float g0 = exp2_fast(m0b - mb), g1 = exp2_fast(m1b - mb);
-      const float la = st.la * f0 + o.la * f1;
-      const float lb = st.lb * g0 + o.lb * g1;
-      const float acc = st.acc * f0 + o.acc * f1;
-      out_la = (ma + log2f(la)) * kLn2;       // LSE_t = m_t + ln l_t (natural log)
-      out_lb = (mb + log2f(lb)) * kLn2;
-      out_kl = acc * kLn2 / la + out_lb - out_la;   // eq:kl-final
-    }
-    kl[ri] = out_kl;
-    lse_a[ri] = out_la;
-    lse_b[ri] = out_lb;
+// Five row statistics with the maxima scaled to the base-2 exponent domain
+// (m = c * raw maximum, -inf when the row has seen no key): the partial state
+// of Sec. 3.3, which merges associatively.
+struct RowPartial {
+  float ma, la, mb, lb, acc;
+};
+
+// Split-K merge (Sec. 3.3) of two partial states of the same row.
+__device__ __forceinline__ RowPartial merge_partials(const RowPartial& x, const RowPartial& y) {
+  RowPartial r;
+  r.ma = fmaxf(x.ma, y.ma);
+  r.mb = fmaxf(x.mb, y.mb);
+  if (r.ma == kNegInf) return RowPartial{kNegInf, 0.f, kNegInf, 0.f, 0.f};
+  const float fx = exp2_fast(x.ma - r.ma), fy = exp2_fast(y.ma - r.ma);
+  const float gx = exp2_fast(x.mb - r.mb), gy = exp2_fast(y.mb - r.mb);
+  r.la = x.la * fx + y.la * fy;
+  r.lb = x.lb * gx + y.lb * gy;
+  r.acc = x.acc * fx + y.acc * fy;
+  return r;
+}
+
+// Merge the states of the two half-waves of each row; lanes of both halves
+// return the row's partial state.
+__device__ __forceinline__ RowPartial halfwave_partial(const RowState& st, float ca, float cb) {
+  auto scaled = [](float c, float m) { return m < kNoKeyRaw ? kNegInf : c * m; };
+  const RowPartial mine{scaled(ca, st.mra), st.la, scaled(cb, st.mrb), st.lb, st.acc};
+  const RowPartial other{__shfl_xor(mine.ma, 32), __shfl_xor(mine.la, 32), __shfl_xor(mine.mb, 32),
+                         __shfl_xor(mine.lb, 32), __shfl_xor(mine.acc, 32)};
+  return merge_partials(mine, other);
+}
+
+// KL (eq:kl-final), LSE_a and LSE_b (natural log) of a row from its complete
+// state: LSE_t = (m_t + log2 l_t) ln 2 and KL = acc ln 2 / l_a + LSE_b - LSE_a.
+__device__ __forceinline__ void write_row(const RowPartial& p, size_t ri, float* __restrict__ kl,
+                                          float* __restrict__ lse_a, float* __restrict__ lse_b) {
+  float out_kl = 0.f, out_la = kNegInf, out_lb = kNegInf;
+  if (p.ma != kNegInf) {
+    out_la = (p.ma + log2f(p.la)) * kLn2;
+    out_lb = (p.mb + log2f(p.lb)) * kLn2;
+    out_kl = p.acc * kLn2 / p.la + out_lb - out_la;
   }
+  kl[ri] = out_kl;
+  lse_a[ri] = out_la;
+  lse_b[ri] = out_lb;
 }
 
 // Row geometry shared by both kernels. Tiles 0 .. tlast hold keys some row of
@@ -255,33 +268,27 @@ struct FwdTraits {
   static constexpr int STAGE = BK * (CA + CB);
   static constexpr int NSTAGE = NSTAGE_;
   // threads that stream the key tiles: 512 when that splits both tensors' chunks evenly, else 256
-  static constexpr int DMA_NT = (NT >= 512 && (BK * CA) % 512 == 0 && (BK * CB) % 512 == 0) ? 512 : 256;
+  static constexpr int DMA_NT = (NT >= 512 && (BK * CA) % 512 == 0 && (BK * CB) % 512 == 0) ? 512 : (NT < 256 ? NT : 256);
   static constexpr int NCH = STAGE / DMA_NT;                // direct-to-LDS loads per streaming thread per tile
   static constexpr int MINB = MINB_;                        // workgroups per CU the registers are sized for
   static_assert(DA % 64 == 0 && DB % 64 == 0, "head dims must be multiples of 64");
   static_assert(NSTAGE >= 2, "tile shape");
 };
 
+// Online pass of one workgroup over key tiles [t_begin, t_end) of the query
+// rows q0 .. q0 + BQ - 1 of head bh; returns the lane's row state (both
+// half-waves merged) and its row index in myq.
 template <class C, bool CAUSAL>
-__global__ void __launch_bounds__(C::NT, C::MINB)
-kl_fwd_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
-              const uint16_t* __restrict__ Qb, const uint16_t* __restrict__ Kb,
-              int NQ, int NK, float ca, float cb,
-              float* __restrict__ kl, float* __restrict__ lse_a, float* __restrict__ lse_b) {
+__device__ __forceinline__ RowPartial fwd_pass(u32x4* smem, const uint16_t* __restrict__ Qa,
+                                               const uint16_t* __restrict__ Ka, const uint16_t* __restrict__ Qb,
+                                               const uint16_t* __restrict__ Kb, int NQ, int NK, float ca, float cb,
+                                               int bh, int q0, int t_begin, int t_end, int& myq) {
   constexpr int DA = C::DA, DB = C::DB, R = C::NSTAGE, BK = C::BK;
-  __shared__ u32x4 smem[R * C::STAGE];
-
   const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int TQ = (NQ + C::BQ - 1) / C::BQ;
-  const int logical = xcd_logical(blockIdx.x, gridDim.x);
-  const int bh = logical / TQ;
-  int qt = logical - bh * TQ;
-  if (CAUSAL) qt = TQ - 1 - qt;   // longest rows first
-  const int q0 = qt * C::BQ;
   const int off = NK - NQ;
   const int qw = q0 + 32 * wave;
-  const int myq = qw + (lane & 31);
+  myq = qw + (lane & 31);
   const int wlast = min(qw + 31, NQ - 1);
 
   int ntiles = (NK + BK - 1) / BK;
@@ -290,6 +297,7 @@ kl_fwd_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
     ntiles = kmax < 0 ? 0 : min(ntiles, kmax / BK + 1);
   }
   const WaveTiles wt = wave_tiles<CAUSAL>(qw, wlast, NQ, NK, ntiles);
+  t_end = min(t_end, ntiles);
   const int kcm = CAUSAL ? myq + off : NK;
 
   bf16x8 qa[DA / 16], qb[DB / 16];
@@ -302,15 +310,15 @@ kl_fwd_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
   const bool streamer = wave < C::DMA_NT / 64;
   RowState st{kNegInf, 0.f, kNegInf, 0.f, 0.f};
   TileCarry tc{};
-  auto stage_of = [&](int t) { return smem + (t % R) * C::STAGE; };
+  auto stage_of = [&](int t) { return smem + ((t - t_begin) % R) * C::STAGE; };
 
-  if (ntiles > 0 && streamer) {
+  if (t_begin < t_end && streamer) {
 #pragma unroll
-    for (int t = 0; t < R - 1; ++t) dma.issue(rka, rkb, t * BK, smem + t * C::STAGE, wave);
-    wait_vmem_le<(R - 2) * C::NCH>();   // tile 0
+    for (int t = 0; t < R - 1; ++t) dma.issue(rka, rkb, (t_begin + t) * BK, smem + t * C::STAGE, wave);
+    wait_vmem_le<(R - 2) * C::NCH>();   // tile t_begin
   }
   barrier_no_fence();
-  for (int t = 0; t < ntiles; ++t) {
+  for (int t = t_begin; t < t_end; ++t) {
     if (streamer) dma.issue(rka, rkb, (t + R - 1) * BK, stage_of(t + R - 1), wave);
     if (t <= wt.tlast) {
       f32x16 sa, sb;
@@ -323,8 +331,73 @@ kl_fwd_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
     barrier_no_fence();                 // ... and for every wave
   }
   wait_vmem();   // no load may still target LDS when the workgroup ends
+  return halfwave_partial(st, ca, cb);
+}
 
-  fwd_finish(st, ca, cb, half, myq < NQ, (size_t)bh * NQ + myq, kl, lse_a, lse_b);
+// Whole key range per workgroup: grid B*H * ceil(N_Q / BQ).
+template <class C, bool CAUSAL>
+__global__ void __launch_bounds__(C::NT, C::MINB)
+kl_fwd_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
+              const uint16_t* __restrict__ Qb, const uint16_t* __restrict__ Kb,
+              int NQ, int NK, float ca, float cb,
+              float* __restrict__ kl, float* __restrict__ lse_a, float* __restrict__ lse_b) {
+  __shared__ u32x4 smem[C::NSTAGE * C::STAGE];
+  const int TQ = (NQ + C::BQ - 1) / C::BQ;
+  const int logical = xcd_logical(blockIdx.x, gridDim.x);
+  const int bh = logical / TQ;
+  int qt = logical - bh * TQ;
+  if (CAUSAL) qt = TQ - 1 - qt;   // longest rows first
+  int myq;
+  const RowPartial p = fwd_pass<C, CAUSAL>(smem, Qa, Ka, Qb, Kb, NQ, NK, ca, cb, bh, qt * C::BQ, 0, 1 << 30, myq);
+  if ((threadIdx.x & 32) == 0 && myq < NQ) write_row(p, (size_t)bh * NQ + myq, kl, lse_a, lse_b);
+}
+
+// Split-K partial pass (Sec. 3.3): grid B*H * ceil(N_Q / BQ) * W; workgroup
+// (head, query tile, w) covers key tiles [w * chunk, (w + 1) * chunk) and
+// writes the five row statistics to part[k][w][B*H*N_Q], k = (m_a, l_a, m_b,
+// l_b, acc), maxima in the base-2 domain.
+template <class C, bool CAUSAL>
+__global__ void __launch_bounds__(C::NT, C::MINB)
+kl_fwd_partial_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
+                      const uint16_t* __restrict__ Qb, const uint16_t* __restrict__ Kb,
+                      int NQ, int NK, float ca, float cb, int W, int chunk, float* __restrict__ part) {
+  __shared__ u32x4 smem[C::NSTAGE * C::STAGE];
+  const int TQ = (NQ + C::BQ - 1) / C::BQ;
+  const int logical = xcd_logical(blockIdx.x, gridDim.x);
+  const int w = logical % W;
+  const int rest = logical / W;
+  const int bh = rest / TQ;
+  const int qt = rest - bh * TQ;
+  int myq;
+  const RowPartial p = fwd_pass<C, CAUSAL>(smem, Qa, Ka, Qb, Kb, NQ, NK, ca, cb, bh, qt * C::BQ, w * chunk,
+                                           (w + 1) * chunk, myq);
+  if ((threadIdx.x & 32) == 0 && myq < NQ) {
+    const size_t rows = (size_t)gridDim.x / W / TQ * NQ;   // B*H*N_Q
+    const size_t ri = (size_t)w * rows + (size_t)bh * NQ + myq;
+    const size_t plane = (size_t)W * rows;
+    part[ri] = p.ma;
+    part[ri + plane] = p.la;
+    part[ri + 2 * plane] = p.mb;
+    part[ri + 3 * plane] = p.lb;
+    part[ri + 4 * plane] = p.acc;
+  }
+}
+
+// Split-K reduce (Sec. 3.3): one thread per row merges its W partial states
+// and writes KL, LSE_a, LSE_b.
+__global__ void __launch_bounds__(256)
+kl_fwd_merge_kernel(const float* __restrict__ part, int W, size_t rows, float* __restrict__ kl,
+                    float* __restrict__ lse_a, float* __restrict__ lse_b) {
+  const size_t ri = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (ri >= rows) return;
+  const size_t plane = (size_t)W * rows;
+  RowPartial acc{kNegInf, 0.f, kNegInf, 0.f, 0.f};
+  for (int w = 0; w < W; ++w) {
+    const size_t i = (size_t)w * rows + ri;
+    acc = merge_partials(acc, RowPartial{part[i], part[i + plane], part[i + 2 * plane], part[i + 3 * plane],
+                                         part[i + 4 * plane]});
+  }
+  write_row(acc, ri, kl, lse_a, lse_b);
 }
 
 // Configuration per head-dim pair: eight waves (256 rows share each key
@@ -332,5 +405,10 @@ kl_fwd_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
 // 128 registers per lane; wider heads take four waves and one workgroup.
 template <int DA, int DB>
 using FwdCfg = typename std::conditional<(DA + DB <= 256), FwdTraits<DA, DB, 2, 2, 8>, FwdTraits<DA, DB, 2, 1, 4>>::type;
+
+// Few query rows per head (decode-like shapes): NW waves per workgroup; four
+// one-wave or two four-wave workgroups per CU (one for wide heads).
+template <int DA, int DB, int NW>
+using FwdSmallCfg = FwdTraits<DA, DB, 2, (DA + DB <= 256) ? (NW == 1 ? 4 : 2) : 1, NW>;
 
 }  // namespace streamkl

@@ -1,22 +1,50 @@
-// Instantiations and launcher of the forward kernels for every head-dim pair.
+// Instantiations and launchers of the forward kernels for every head-dim pair.
 #include "kl_fwd.hpp"
 #include "kl_launch.hpp"
 
 namespace streamkl {
 
-template <int DA, int DB, bool CAUSAL>
-static hipError_t run_fwd(const FwdArgs& a) {
-  using C = FwdCfg<DA, DB>;
+// Waves per workgroup follow the query rows of a head: one wave for at most 32
+// rows, four for at most 128, otherwise the default configuration.
+template <int DA, int DB, bool CAUSAL, class C>
+static hipError_t run_cfg(const FwdArgs& a, int W, float* part) {
   const int tq = (a.NQ + C::BQ - 1) / C::BQ;
-  const dim3 grid((unsigned)((long long)a.BH * tq));
-  hipLaunchKernelGGL((kl_fwd_kernel<C, CAUSAL>), grid, dim3(C::NT), 0, a.stream,
-                     a.Qa, a.Ka, a.Qb, a.Kb, a.NQ, a.NK, a.ca, a.cb, a.kl, a.lse_a, a.lse_b);
+  if (W <= 1) {
+    const dim3 grid((unsigned)((long long)a.BH * tq));
+    hipLaunchKernelGGL((kl_fwd_kernel<C, CAUSAL>), grid, dim3(C::NT), 0, a.stream,
+                       a.Qa, a.Ka, a.Qb, a.Kb, a.NQ, a.NK, a.ca, a.cb, a.kl, a.lse_a, a.lse_b);
+    return hipGetLastError();
+  }
+  const int nkt = (a.NK + C::BK - 1) / C::BK;
+  const int chunk = (nkt + W - 1) / W;
+  const dim3 grid((unsigned)((long long)a.BH * tq * W));
+  hipLaunchKernelGGL((kl_fwd_partial_kernel<C, CAUSAL>), grid, dim3(C::NT), 0, a.stream,
+                     a.Qa, a.Ka, a.Qb, a.Kb, a.NQ, a.NK, a.ca, a.cb, W, chunk, part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const size_t rows = (size_t)a.BH * a.NQ;
+  hipLaunchKernelGGL(kl_fwd_merge_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, a.stream,
+                     part, W, rows, a.kl, a.lse_a, a.lse_b);
   return hipGetLastError();
 }
 
-hipError_t launch_fwd(int da, int db, bool causal, const FwdArgs& a) {
+template <int DA, int DB, bool CAUSAL>
+static hipError_t run_fwd(const FwdArgs& a, int W, float* part) {
+  if (a.NQ <= 32) return run_cfg<DA, DB, CAUSAL, FwdSmallCfg<DA, DB, 1>>(a, W, part);
+  if constexpr (DA + DB <= 256)
+    if (a.NQ <= 128) return run_cfg<DA, DB, CAUSAL, FwdSmallCfg<DA, DB, 4>>(a, W, part);
+  return run_cfg<DA, DB, CAUSAL, FwdCfg<DA, DB>>(a, W, part);
+}
+
+int fwd_rows_per_workgroup(int da, int db, int n_q) {
+  if (n_q <= 32) return 32;
+  if (da + db <= 256) return n_q <= 128 ? 128 : 256;
+  return 128;
+}
+
+hipError_t launch_fwd(int da, int db, bool causal, const FwdArgs& a, int W, float* part) {
 #define STREAMKL_CASE(DA, DB) \
-  if (da == DA && db == DB) return causal ? run_fwd<DA, DB, true>(a) : run_fwd<DA, DB, false>(a);
+  if (da == DA && db == DB) return causal ? run_fwd<DA, DB, true>(a, W, part) : run_fwd<DA, DB, false>(a, W, part);
   STREAMKL_FOR_EACH_DIM_PAIR(STREAMKL_CASE)
 #undef STREAMKL_CASE
   return hipErrorInvalidValue;

@@ -28,7 +28,11 @@ struct BwdArgs {
 
 // Each returns hipErrorInvalidValue for a head-dim pair it does not hold,
 // otherwise the status of the launch (hipGetLastError).
-hipError_t launch_fwd(int da, int db, bool causal, const FwdArgs& a);
+// W <= 1: one pass over all keys. W > 1: split-K (Sec. 3.3) with W key chunks;
+// part holds 5 * W * BH * NQ floats of partial row statistics.
+hipError_t launch_fwd(int da, int db, bool causal, const FwdArgs& a, int W, float* part);
+// Query rows per workgroup of the forward for these head dims and rows per head.
+int fwd_rows_per_workgroup(int da, int db, int n_q);
 hipError_t launch_bwd_dq(int da, int db, bool causal, int mode, const BwdArgs& a);
 hipError_t launch_bwd_dk(int da, int db, bool causal, int mode, const BwdArgs& a);
 hipError_t launch_bwd_dq_m1(int da, int db, bool causal, const BwdArgs& a);

@@ -60,12 +60,26 @@ hipError_t zero_fill(float* p, size_t n, hipStream_t stream) {
 
 }  // namespace
 
-extern "C" int streamkl_fwd(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H, int N_Q,
-                            int N_K, int d1, int d2, float s1, float s2, int causal, int direction, float* kl,
-                            float* lse1, float* lse2, hipStream_t stream) {
+namespace {
+
+int fwd_common(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H, int N_Q, int N_K, int d1,
+               int d2, float s1, float s2, int causal, int direction, int splits, void* workspace,
+               size_t workspace_bytes, float* kl, float* lse1, float* lse2, hipStream_t stream) {
   bool empty = false;
   const int st = check_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, &empty);
-  if (st != STREAMKL_OK || empty) return st;
+  if (st != STREAMKL_OK) return st;
+  if (splits < 1) return STREAMKL_ERR_INVALID_ARG;
+  if (splits > 1) {
+    const long long rows = (long long)B * H * N_Q;
+    const long long grid = (long long)B * H *
+                           ((N_Q + streamkl::fwd_rows_per_workgroup(d1, d2, N_Q) - 1) /
+                            streamkl::fwd_rows_per_workgroup(d1, d2, N_Q)) * splits;
+    if (grid > kMaxGrid || rows * splits > (1LL << 40)) return STREAMKL_ERR_UNSUPPORTED;
+    if (!empty && (!workspace || !aligned(workspace, 4) ||
+                   workspace_bytes < streamkl_fwd_split_workspace_bytes(B, H, N_Q, splits)))
+      return STREAMKL_ERR_INVALID_ARG;
+  }
+  if (empty) return STREAMKL_OK;
   if (!kl || !lse1 || !lse2) return STREAMKL_ERR_INVALID_ARG;
   if (!aligned(kl, 4) || !aligned(lse1, 4) || !aligned(lse2, 4)) return STREAMKL_ERR_INVALID_ARG;
   const bool rev = direction == STREAMKL_KL_REV;
@@ -83,7 +97,42 @@ extern "C" int streamkl_fwd(const void* Q1, const void* K1, const void* Q2, cons
   a.lse_a = rev ? lse2 : lse1;
   a.lse_b = rev ? lse1 : lse2;
   a.stream = stream;
-  return hip_status(streamkl::launch_fwd(rev ? d2 : d1, rev ? d1 : d2, causal == 1, a));
+  return hip_status(streamkl::launch_fwd(rev ? d2 : d1, rev ? d1 : d2, causal == 1, a, splits,
+                                         static_cast<float*>(workspace)));
+}
+
+}  // namespace
+
+extern "C" int streamkl_fwd(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H, int N_Q,
+                            int N_K, int d1, int d2, float s1, float s2, int causal, int direction, float* kl,
+                            float* lse1, float* lse2, hipStream_t stream) {
+  return fwd_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, 1, nullptr, 0, kl, lse1,
+                    lse2, stream);
+}
+
+extern "C" int streamkl_fwd_split(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H,
+                                  int N_Q, int N_K, int d1, int d2, float s1, float s2, int causal, int direction,
+                                  int splits, void* workspace, size_t workspace_bytes, float* kl, float* lse1,
+                                  float* lse2, hipStream_t stream) {
+  return fwd_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, splits, workspace,
+                    workspace_bytes, kl, lse1, lse2, stream);
+}
+
+extern "C" size_t streamkl_fwd_split_workspace_bytes(int B, int H, int N_Q, int splits) {
+  if (B < 0 || H < 0 || N_Q < 0 || splits <= 1) return 0;
+  return (size_t)20 * (size_t)splits * (size_t)B * (size_t)H * (size_t)N_Q;
+}
+
+extern "C" int streamkl_fwd_split_count(int B, int H, int N_Q, int N_K, int d1, int d2) {
+  if (B < 0 || H < 0 || N_Q < 0 || N_K < 0) return 0;
+  if (!supported_dim(d1) || !supported_dim(d2)) return 0;
+  constexpr long long kTarget = 512;   // two workgroups per CU on 256 CUs
+  const int bq = streamkl::fwd_rows_per_workgroup(d1, d2, N_Q);
+  const long long base = (long long)B * H * ((N_Q + bq - 1) / bq);
+  if (base == 0 || base >= kTarget) return 1;
+  const long long tiles = (N_K + 31LL) / 32;
+  const long long w = kTarget / base < tiles ? kTarget / base : tiles;
+  return w < 1 ? 1 : (int)w;
 }
 
 extern "C" int streamkl_bwd(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H, int N_Q,

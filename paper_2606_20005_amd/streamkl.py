@@ -6,6 +6,7 @@ current HIP stream. Importing this module fails loudly when the library has
 not been built; there is no fallback implementation.
 
     kl, lse1, lse2 = fwd(q1, k1, q2, k2, s1, s2, causal, direction)
+    kl, lse1, lse2 = fwd_split(q1, k1, q2, k2, s1, s2, causal, direction, splits="auto")
     dQ1, dK1, dQ2, dK2 = bwd(q1, k1, q2, k2, kl, lse1, lse2, dkl, ..., want=("dq2", "dk2"))
     loss = attention_kl(q1, k1, q2, k2, causal=True).mean(); loss.backward()
 """
@@ -21,7 +22,8 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libstreamkl
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP = 0, 1, 2, 3
 FWD, REV = 0, 1
-ENTRY_POINTS = ("streamkl_fwd", "streamkl_bwd", "streamkl_strerror", "streamkl_version",
+ENTRY_POINTS = ("streamkl_fwd", "streamkl_bwd", "streamkl_fwd_split", "streamkl_fwd_split_workspace_bytes",
+                "streamkl_fwd_split_count", "streamkl_strerror", "streamkl_version",
                 "streamkl_supported_head_dim")
 
 
@@ -35,6 +37,13 @@ def _load():
     lib.streamkl_fwd.restype = i
     lib.streamkl_bwd.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, f, f, i, i, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.streamkl_bwd.restype = i
+    sz = ctypes.c_size_t
+    lib.streamkl_fwd_split.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, f, f, i, i, i, vp, sz, vp, vp, vp, vp]
+    lib.streamkl_fwd_split.restype = i
+    lib.streamkl_fwd_split_workspace_bytes.argtypes = [i, i, i, i]
+    lib.streamkl_fwd_split_workspace_bytes.restype = sz
+    lib.streamkl_fwd_split_count.argtypes = [i, i, i, i, i, i]
+    lib.streamkl_fwd_split_count.restype = i
     lib.streamkl_strerror.argtypes = [i]
     lib.streamkl_strerror.restype = ctypes.c_char_p
     lib.streamkl_version.argtypes = []
@@ -127,6 +136,44 @@ def fwd(q1, k1, q2, k2, s1=None, s2=None, causal=False, direction=FWD, out=None)
     return kl, lse1, lse2
 
 
+def split_count(B, H, n_q, n_k, d1, d2) -> int:
+    """streamkl_fwd_split_count: the adaptive split count of Sec. 3.3 (0 for invalid arguments)."""
+    return int(lib.streamkl_fwd_split_count(int(B), int(H), int(n_q), int(n_k), int(d1), int(d2)))
+
+
+def split_workspace_bytes(B, H, n_q, splits) -> int:
+    """streamkl_fwd_split_workspace_bytes: workspace the split-K forward needs."""
+    return int(lib.streamkl_fwd_split_workspace_bytes(int(B), int(H), int(n_q), int(splits)))
+
+
+def fwd_split(q1, k1, q2, k2, s1=None, s2=None, causal=False, direction=FWD, splits="auto", out=None,
+              workspace=None):
+    """streamkl_fwd_split: the split-K forward; returns (kl, lse1, lse2) like fwd.
+
+    splits: an int >= 1 or "auto" (split_count). The workspace is allocated
+    here unless ``workspace`` (a device tensor of at least split_workspace_bytes
+    bytes) is given.
+    """
+    B, H, NQ, NK, d1, d2 = _check_inputs(q1, k1, q2, k2)
+    s1, s2 = _scales(s1, s2, d1, d2)
+    dev = q1.device
+    w = split_count(B, H, NQ, NK, d1, d2) if splits == "auto" else int(splits)
+    if out is None:
+        out = tuple(torch.empty((B, H, NQ), dtype=torch.float32, device=dev) for _ in range(3))
+    kl, lse1, lse2 = (_f32_rows(t, (B, H, NQ), dev, n) for t, n in zip(out, ("kl", "lse1", "lse2")))
+    need = split_workspace_bytes(B, H, NQ, w)
+    if workspace is None:
+        workspace = torch.empty(max(need, 4), dtype=torch.uint8, device=dev)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    with torch.cuda.device(dev):
+        st = lib.streamkl_fwd_split(_p(q1), _p(k1), _p(q2), _p(k2), B, H, NQ, NK, d1, d2, s1, s2,
+                                    int(bool(causal)), _direction(direction), w, _p(workspace), ws_bytes,
+                                    _p(kl), _p(lse1), _p(lse2), _stream(dev))
+    if st != OK:
+        raise StreamKLError(st, "streamkl_fwd_split")
+    return kl, lse1, lse2
+
+
 def bwd(q1, k1, q2, k2, kl, lse1, lse2, dkl=None, s1=None, s2=None, causal=False, direction=FWD,
         want=("dq2", "dk2"), out=None):
     """streamkl_bwd: returns (dQ1, dK1, dQ2, dK2), float32, None where not requested.
@@ -167,7 +214,8 @@ def bwd(q1, k1, q2, k2, kl, lse1, lse2, dkl=None, s1=None, s2=None, causal=False
 class _AttentionKL(torch.autograd.Function):
     @staticmethod
     def forward(ctx, q1, k1, q2, k2, s1, s2, causal, direction):
-        kl, lse1, lse2 = fwd(q1, k1, q2, k2, s1, s2, causal, direction)
+        # the adaptive split count is 1 (the single-pass kernel) unless the heads have few query rows
+        kl, lse1, lse2 = fwd_split(q1, k1, q2, k2, s1, s2, causal, direction, splits="auto")
         ctx.save_for_backward(q1, k1, q2, k2, kl, lse1, lse2)
         ctx.cfg = (s1, s2, causal, direction)
         ctx.mark_non_differentiable(lse1, lse2)

@@ -95,3 +95,48 @@ def test_python_binding_rejects_cpu_tensors(sk):
     x = torch.zeros((1, 1, 4, 64), dtype=torch.bfloat16)
     with pytest.raises(ValueError):
         sk.fwd(x, x, x, x)
+
+
+def split_call(sk, **kw):
+    a = dict(Q1=FAKE, K1=FAKE, Q2=FAKE, K2=FAKE, B=1, H=2, NQ=16, NK=4096, d1=64, d2=64, s1=0.125, s2=0.125,
+             causal=0, direction=0, splits=4, ws=FAKE, ws_bytes=1 << 20, kl=FAKE, lse1=FAKE, lse2=FAKE,
+             stream=None)
+    a.update(kw)
+    return sk.lib.streamkl_fwd_split(a["Q1"], a["K1"], a["Q2"], a["K2"], a["B"], a["H"], a["NQ"], a["NK"], a["d1"],
+                                     a["d2"], a["s1"], a["s2"], a["causal"], a["direction"], a["splits"], a["ws"],
+                                     a["ws_bytes"], a["kl"], a["lse1"], a["lse2"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(splits=0), 1), (dict(splits=-2), 1), (dict(ws=None), 1), (dict(ws=ctypes.c_void_p(0x100002)), 1),
+    (dict(ws_bytes=20 * 4 * 2 * 16 - 1), 1), (dict(kl=None), 1), (dict(Q1=None), 1), (dict(d2=96), 2),
+    (dict(B=0), 0), (dict(NQ=0, ws=None, Q1=None, Q2=None, kl=None, lse1=None, lse2=None), 0),
+])
+def test_split_argument_checks(sk, kw, expect):
+    assert split_call(sk, **kw) == expect
+
+
+def test_split_workspace_bytes(sk):
+    # five fp32 row statistics per split, per row (m1, l1, m2, l2, acc)
+    assert sk.split_workspace_bytes(2, 3, 17, 5) == 20 * 5 * 2 * 3 * 17
+    assert sk.split_workspace_bytes(2, 3, 17, 1) == 0
+    assert sk.split_workspace_bytes(-1, 3, 17, 4) == 0
+
+
+def test_split_count_follows_the_adaptive_rule(sk):
+    """W = 1 once the single-pass grid reaches the target of 512 workgroups,
+    otherwise floor(512 / P_base) capped by the number of 32-key tiles."""
+    # 16 heads of 16 query rows (one 32-row workgroup each) over 64K keys: 512 / 16
+    assert sk.split_count(16, 1, 16, 65536, 128, 128) == 32
+    # one query row, 4 heads: 512 / 4 = 128 chunks
+    assert sk.split_count(1, 4, 1, 1 << 20, 64, 64) == 128
+    # a 16K x 16K head set already launches 2048 workgroups of 256 rows
+    assert sk.split_count(1, 32, 16384, 16384, 128, 128) == 1
+    # 8 heads of 8192 rows: 256 workgroups of 256 rows -> 2
+    assert sk.split_count(1, 8, 8192, 131072, 192, 64) == 2
+    # capped by the tiles of a short key range: 40 keys are 2 tiles
+    assert sk.split_count(1, 1, 1, 40, 128, 128) == 2
+    assert sk.split_count(1, 1, 1, 0, 128, 128) == 1
+    # invalid or unsupported
+    assert sk.split_count(-1, 1, 1, 1, 128, 128) == 0
+    assert sk.split_count(1, 1, 1, 1, 96, 128) == 0
