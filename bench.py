@@ -150,7 +150,7 @@ def run_workload(sk, w, causal, steps, warmup):
 
 def split_k_figures(sk, reps=10):
     """Split-K forward (Sec. 3.3) against the single pass on decode-like shapes:
-    16 heads of N_Q in {1, 16, 64} rows over N_K = 65536 keys, d1 = d2 = 128,
+    16 heads of N_Q in {1, 16, 32, 64} rows over N_K = 65536 keys, d1 = d2 = 128,
     non-causal (the shape family of the paper's split-K ablation). Inputs are
     seeded N(0,1) drawn on the device; HIP events over `reps` launches each."""
     import torch
@@ -161,7 +161,7 @@ def split_k_figures(sk, reps=10):
     k2 = torch.randn((B, H, NK, D), generator=gen, device="cuda").to(torch.bfloat16)
     s = D ** -0.5
     out = []
-    for nq in (1, 16, 64):
+    for nq in (1, 16, 32, 64):
         q1 = torch.randn((B, H, nq, D), generator=gen, device="cuda").to(torch.bfloat16)
         q2 = torch.randn((B, H, nq, D), generator=gen, device="cuda").to(torch.bfloat16)
         res = {"n_q": nq}
@@ -179,10 +179,11 @@ def split_k_figures(sk, reps=10):
         res["splits"] = sk.split_count(B, H, nq, NK, D, D)
         res["speedup"] = round(res["single_pass_ms"] / res["split_ms"], 2)
         res["split_tflops"] = round(2 * 2 * D * B * H * nq * NK / (res["split_ms"] * 1e-3) / 1e12, 2)
+        res["split_k_stream_tbps"] = round(2 * D * 2 * B * H * NK / (res["split_ms"] * 1e-3) / 1e12, 2)
         out.append(res)
     del k1, k2
     torch.cuda.empty_cache()
-    return {"workload": f"B={B} H={H} N_K={NK} d1=d2={D} non-causal, N_Q in (1, 16, 64)", "rows": out}
+    return {"workload": f"B={B} H={H} N_K={NK} d1=d2={D} non-causal, N_Q in (1, 16, 32, 64)", "rows": out}
 
 
 def summarize(w, causal, ms):
