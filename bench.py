@@ -12,9 +12,10 @@ d1=d2=128, s=1/sqrt(128), non-causal, student Q2 = bf16(Q1 + 0.3 eps), K2 = K1.
 Prints ONE JSON line. The 64K causal long-context figures (d1=128, d2=64,
 outlier channels) ride along in "long_context" unless --no-64k, and the
 split-K forward on decode-like shapes (16 heads of 1-64 query rows over 64K
-keys) in "split_k" unless --no-split.
+keys) in "split_k" unless --no-split, and the separate against the fused
+backward on the same shapes in "fused_bwd" unless --no-fused.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-64k] [--no-cpu-baseline] [--no-split]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-64k] [--no-cpu-baseline] [--no-split] [--no-fused]
 """
 from __future__ import annotations
 
@@ -186,6 +187,51 @@ def split_k_figures(sk, reps=10):
     return {"workload": f"B={B} H={H} N_K={NK} d1=d2={D} non-causal, N_Q in (1, 16, 32, 64)", "rows": out}
 
 
+def fused_bwd_figures(sk, reps=10):
+    """Backward strategies of Sec. 4.2 on the same decode-like shapes as the
+    split-K figures (16 heads, N_K = 65536, d1 = d2 = 128, non-causal, student
+    gradients dQ2 and dK2), plus 512 query rows near the measured crossover:
+    the separate dQ/dK kernels against the fused key-owned kernel with atomic
+    dQ, and the strategy the adaptive rule picks. HIP events over `reps`
+    calls each."""
+    import torch
+    B, H, NK, D = 16, 1, 65536, 128
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(2606200050 + 7)
+    mk = lambda n: torch.randn((B, H, n, D), generator=gen, device="cuda").to(torch.bfloat16)  # noqa: E731
+    k1, k2 = mk(NK), mk(NK)
+    s = D ** -0.5
+    out = []
+    for nq in (1, 16, 32, 64, 512):
+        q1, q2 = mk(nq), mk(nq)
+        kl, l1, l2 = sk.fwd(q1, k1, q2, k2, s, s, False, 0)
+        g = torch.full((B, H, nq), 1.0 / (B * H * nq), device="cuda")
+        grads = {"dq2": torch.empty((B, H, nq, D), device="cuda"), "dk2": torch.empty((B, H, NK, D), device="cuda")}
+        res = {"n_q": nq}
+        for strat in ("separate", "fused"):
+            fn = lambda: sk.bwd(q1, k1, q2, k2, kl, l1, l2, g, s, s, False, 0, out=grads, strategy=strat)  # noqa: E731
+            fn()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            res[strat + "_ms"] = round(e0.elapsed_time(e1) / reps, 4)
+        res["speedup"] = round(res["separate_ms"] / res["fused_ms"], 2)
+        res["auto_picks"] = sk.bwd_choose(B, H, nq, NK, D, D)
+        # compulsory bytes of the fused pass: K1, K2 read once, dK2 written, dQ2 added
+        byts = B * H * (2 * NK * D * 2 + NK * D * 4 + 2 * nq * D * 2 + nq * D * 4)
+        res["fused_hbm_tbps"] = round(byts / (res["fused_ms"] * 1e-3) / 1e12, 2)
+        out.append(res)
+        del q1, q2, kl, l1, l2, g, grads
+    del k1, k2
+    torch.cuda.empty_cache()
+    return {"workload": f"B={B} H={H} N_K={NK} d1=d2={D} non-causal, dQ2 + dK2, N_Q in (1, 16, 32, 64, 512)",
+            "rows": out}
+
+
 def summarize(w, causal, ms):
     P = pairs(w, causal)
     f = flops_per_pair(w)
@@ -238,6 +284,7 @@ def main():
     ap.add_argument("--no-64k", action="store_true", help="skip the 64K long-context figures")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-split", action="store_true", help="skip the split-K decode-shape figures")
+    ap.add_argument("--no-fused", action="store_true", help="skip the fused-backward decode-shape figures")
     ap.add_argument("--causal", action="store_true", help="run the 16K workload with causal masking")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run one 1 GiB device copy (reference kernel for HBM counters)")
@@ -304,6 +351,8 @@ def main():
             "naive_p1_p2_bytes": 2 * 2 * P_l, "kl_mean": kl_l}
     if not a.no_split:
         res["split_k"] = split_k_figures(sk)
+    if not a.no_fused:
+        res["fused_bwd"] = fused_bwd_figures(sk)
     if a.copy_calibration:
         x = torch.empty(1 << 28, dtype=torch.float32, device="cuda")   # 1 GiB
         y = torch.empty_like(x)

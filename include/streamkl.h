@@ -35,7 +35,9 @@
  *   belong to (Q1,K1,s1) / (Q2,K2,s2).
  * - Supported head dims: d1, d2 in {64, 128, 192, 256}.
  * - B, H, N_Q, N_K >= 0; a zero extent is a valid call that launches
- *   nothing (N_K = 0 with N_Q > 0 makes every row empty).
+ *   nothing (N_K = 0 with N_Q > 0 makes every row empty). One head's rows
+ *   of any tensor must span less than 4 GiB as fp32 (N * max(d1, d2) * 4 <
+ *   2^32), else STREAMKL_ERR_UNSUPPORTED.
  * - Work is enqueued on `stream` (NULL = the default stream) and the call
  *   returns before it completes. Asynchronous faults surface at the caller's
  *   next synchronisation, as usual for HIP.
@@ -64,6 +66,21 @@ typedef enum {
   STREAMKL_KL_FWD = 0, /* L = KL(P1 || P2), eq:kl-def                */
   STREAMKL_KL_REV = 1  /* L = KL(P2 || P1), the two roles swapped    */
 } streamkl_direction;
+
+/* Backward kernel strategies of Sec. 4.2 ("GPU Kernel Design"). */
+typedef enum {
+  STREAMKL_BWD_AUTO = 0,     /* adaptive selection (streamkl_bwd_choose)          */
+  STREAMKL_BWD_SEPARATE = 1, /* query-owned dQ kernel + key-owned dK kernel        */
+  STREAMKL_BWD_FUSED = 2     /* one key-owned kernel, dQ added with fp32 atomics   */
+} streamkl_bwd_strategy;
+
+/* Gradient request bits of streamkl_bwd_choose. */
+enum {
+  STREAMKL_GRAD_DQ1 = 1,
+  STREAMKL_GRAD_DK1 = 2,
+  STREAMKL_GRAD_DQ2 = 4,
+  STREAMKL_GRAD_DK2 = 8
+};
 
 /*
  * Forward pass (Algorithm 1, Sec. 3.2; eq:kl-final): one tiled pass over the
@@ -94,7 +111,8 @@ int streamkl_fwd(const void* Q1, const void* K1, const void* Q2, const void* K2,
  * dQ1, dK1, dQ2, dK2: each NULL (not computed) or written in full
  * (overwritten, never accumulated into). At least one must be non-NULL.
  * dQ tiles are owned by query blocks and dK tiles by key blocks, so no
- * atomics are used and results are bitwise reproducible run to run.
+ * atomics are used and results are bitwise reproducible run to run (the
+ * separate-kernel strategy of Sec. 4.2; streamkl_bwd_ex offers the fused one).
  */
 int streamkl_bwd(const void* Q1, const void* K1, const void* Q2, const void* K2,
                  int B, int H, int N_Q, int N_K, int d1, int d2,
@@ -103,6 +121,46 @@ int streamkl_bwd(const void* Q1, const void* K1, const void* Q2, const void* K2,
                  const float* dkl,
                  float* dQ1, float* dK1, float* dQ2, float* dK2,
                  hipStream_t stream);
+
+/*
+ * Backward pass with a choice of kernel strategy (Sec. 4.2, "Separate dQ/dK
+ * Kernels", "Fused Backward Kernel", "Adaptive Strategy Selection").
+ * Arguments, outputs and errors are those of streamkl_bwd, plus `strategy`:
+ *   STREAMKL_BWD_SEPARATE  exactly streamkl_bwd (bitwise reproducible).
+ *   STREAMKL_BWD_FUSED     one kernel over (batch*head, 128-key blocks): each
+ *                          workgroup recomputes its key block against every
+ *                          query tile once, writes dK for its keys and adds
+ *                          its share of dQ with fp32 atomic adds. dQ is first
+ *                          zeroed on `stream`. The summation order of dQ is
+ *                          not fixed, so dQ may differ between runs in the
+ *                          last bits (dK does not). Returns
+ *                          STREAMKL_ERR_UNSUPPORTED when a dQ is requested
+ *                          and the fused kernel's working set does not fit
+ *                          in LDS for these head dims (only when gradients
+ *                          of both distributions are requested and
+ *                          d1 + d2 > 320).
+ *   STREAMKL_BWD_AUTO      the strategy streamkl_bwd_choose returns.
+ * With no dQ requested every strategy runs the dK kernel alone.
+ */
+int streamkl_bwd_ex(const void* Q1, const void* K1, const void* Q2, const void* K2,
+                    int B, int H, int N_Q, int N_K, int d1, int d2,
+                    float s1, float s2, int causal, int direction,
+                    const float* kl, const float* lse1, const float* lse2,
+                    const float* dkl,
+                    float* dQ1, float* dK1, float* dQ2, float* dK2,
+                    int strategy, hipStream_t stream);
+
+/*
+ * Adaptive strategy selection (Sec. 4.2): with T_Q and T_K the numbers of
+ * 128-row query and key tiles per head, returns STREAMKL_BWD_FUSED when
+ * T_Q * C <= T_K (dQ small next to dK, so its atomics stay cheap) with C = 8,
+ * T_Q <= 4, and the fused kernel exists for the request; else
+ * STREAMKL_BWD_SEPARATE. The constants were measured on MI355X: there the
+ * fused kernel loses beyond 512 query rows at any N_K. `grads` is an OR of
+ * STREAMKL_GRAD_* bits. Returns 0 for invalid or unsupported arguments.
+ */
+int streamkl_bwd_choose(int B, int H, int N_Q, int N_K, int d1, int d2,
+                        int causal, int direction, int grads);
 
 /*
  * Split-K forward (Sec. 3.3, "Split-K variant" and "Adaptive split

@@ -66,6 +66,56 @@ __device__ __forceinline__ RowStats load_row_stats(const float* kl, const float*
   return s;
 }
 
+// Saved values (LSE_a, LSE_b, L and, when given, g) of 64 consecutive query
+// rows of one head, brought into LDS raw[4][64] by direct-to-LDS dword loads
+// that travel with the tile loads (rows past N_Q read as zeros). One wave
+// issues them; after its wait for the tile, stage_row_stats turns the 32 rows
+// of the tile into the form the inner loop uses.
+struct RowsDma {
+  rsrc_t r_la, r_lb, r_kl, r_g;
+  bool has_g;
+  __device__ __forceinline__ RowsDma(const float* kl, const float* lse_a, const float* lse_b, const float* g,
+                                     size_t head_row0, int NQ) {
+    const uint32_t bytes = (uint32_t)NQ * 4u;
+    r_la = make_rsrc(lse_a + head_row0, bytes);
+    r_lb = make_rsrc(lse_b + head_row0, bytes);
+    r_kl = make_rsrc(kl + head_row0, bytes);
+    has_g = g != nullptr;
+    r_g = make_rsrc(has_g ? g + head_row0 : kl + head_row0, bytes);
+  }
+  __device__ __forceinline__ void issue(int row0, float (*raw)[64], int lane) const {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const uint32_t off = (uint32_t)(row0 + lane) * 4u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r_la, (lds_void*)raw[0], 4, off, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r_lb, (lds_void*)raw[1], 4, off, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r_kl, (lds_void*)raw[2], 4, off, 0, 0, 0);
+    if (has_g) __builtin_amdgcn_raw_ptr_buffer_load_lds(r_g, (lds_void*)raw[3], 4, off, 0, 0, 0);
+#endif
+  }
+};
+
+// Statistics of a streamed 32-row tile in LDS: [lsa2, lsb2, g, dl][row].
+template <int BS>
+__device__ __forceinline__ void stage_row_stats(const float (*raw)[64], int r0, int NQ, bool has_g,
+                                                f32x4 (&dst)[4][BS / 4], int tid) {
+  if (tid < BS) {
+    RowStats s{0.f, 0.f, 0.f, 0.f};
+    const float la = raw[0][tid];
+    if (r0 + tid < NQ && la != kNegInf) {   // padding and rows with no allowed key contribute nothing
+      const float lb = raw[1][tid];
+      s.lsa2 = la * kLog2e;
+      s.lsb2 = lb * kLog2e;
+      s.g = has_g ? raw[3][tid] : 1.f;
+      s.dl = (la - lb) + raw[2][tid];
+    }
+    float* p = reinterpret_cast<float*>(&dst[0][0]);
+    p[0 * BS + tid] = s.lsa2;
+    p[1 * BS + tid] = s.lsb2;
+    p[2 * BS + tid] = s.g;
+    p[3 * BS + tid] = s.dl;
+  }
+}
+
 // Logit gradients of one element (raw dot products ra, rb).
 template <bool WANT_A, bool WANT_B>
 __device__ __forceinline__ void dlogits(float ra, float rb, bool ok, float ca, float cb, float sa, float sb,
@@ -84,22 +134,19 @@ __device__ __forceinline__ void dlogits(float ra, float rb, bool ok, float ca, f
 }
 
 // ----------------------------------------------------------------------------
-// One streamed tile of one wave, shared by both kernels. The wave owns 32
-// resident rows (queries for dQ, keys for dK) held as MFMA B operands ra_op,
-// rb_op; the stage holds 32 streamed rows of A and B. S = stage_rows x
+// One streamed tile of one wave, shared by all backward kernels. The wave owns
+// 32 resident rows (queries for dQ, keys for dK) held as MFMA B operands
+// ra_op, rb_op; the stage holds 32 streamed rows of A and B. S = stage_rows x
 // resident^T, so in the result lane l owns resident row l % 32 and 16 streamed
-// rows. stats(i) returns the row statistics of element i and ok(i) whether
-// element i is an allowed pair. The gradient tiles accumulate
-//   grad[resident][d] += sum_streamed dS[streamed][resident] * X[streamed][d]
-// with X the streamed rows of the stage (transpose reads).
+// rows (register i: streamed row 8 (i / 4) + 4 (l / 32) + i % 4). stats(i)
+// returns the row statistics of element i and ok(i) whether element i is an
+// allowed pair.
 // ----------------------------------------------------------------------------
-template <int DA, int DB, int MODE, bool MASK, typename StatsFn, typename OkFn>
-__device__ __forceinline__ void bwd_tile(const u32x4* stage, const bf16x8 (&ra_op)[DA / 16],
-                                         const bf16x8 (&rb_op)[DB / 16],
-                                         f32x16 (&ga)[(MODE & 2) ? DA / 32 : 1],
-                                         f32x16 (&gb)[(MODE & 1) ? DB / 32 : 1],
-                                         float ca, float cb, float sa, float sb, int lane,
-                                         StatsFn stats, OkFn ok) {
+// ra_op(ks), rb_op(ks) return the resident operands of k-step ks (16 columns).
+template <int DA, int DB, int MODE, bool MASK, typename OpA, typename OpB, typename StatsFn, typename OkFn>
+__device__ __forceinline__ void bwd_dlogits_tile(const u32x4* stage, OpA ra_op, OpB rb_op, float ca, float cb,
+                                                 float sa, float sb, int lane, StatsFn stats, OkFn ok,
+                                                 float (&dsa)[16], float (&dsb)[16]) {
   using C = BwdCfg<DA, DB, MODE>;
   const int half = lane >> 5;
   const u32x4* ta = stage;
@@ -107,15 +154,28 @@ __device__ __forceinline__ void bwd_tile(const u32x4* stage, const bf16x8 (&ra_o
   const int r = lane & 31;
   f32x16 s_a = zero16(), s_b = zero16();
 #pragma unroll
-  for (int ks = 0; ks < DA / 16; ++ks) s_a = mfma32(lds_row8<C::CA>(ta, r, 2 * ks + half), ra_op[ks], s_a);
+  for (int ks = 0; ks < DA / 16; ++ks) s_a = mfma32(lds_row8<C::CA>(ta, r, 2 * ks + half), ra_op(ks), s_a);
 #pragma unroll
-  for (int ks = 0; ks < DB / 16; ++ks) s_b = mfma32(lds_row8<C::CB>(tb, r, 2 * ks + half), rb_op[ks], s_b);
-  float dsa[16], dsb[16];
+  for (int ks = 0; ks < DB / 16; ++ks) s_b = mfma32(lds_row8<C::CB>(tb, r, 2 * ks + half), rb_op(ks), s_b);
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     const RowStats rs = stats(i);
     dlogits<C::WANT_A, C::WANT_B>(s_a[i], s_b[i], MASK ? ok(i) : true, ca, cb, sa, sb, rs, dsa[i], dsb[i]);
   }
+}
+
+// Gradient tiles of the resident rows from the logit gradients of one tile:
+//   grad[resident][d] += sum_streamed dS[streamed][resident] * X[streamed][d]
+// with X the streamed rows of the stage (transpose reads). dS, rounded to
+// bf16, is the A operand as it lies in the registers.
+template <int DA, int DB, int MODE>
+__device__ __forceinline__ void bwd_grad_tile(const u32x4* stage, const float (&dsa)[16], const float (&dsb)[16],
+                                              f32x16 (&ga)[(MODE & 2) ? DA / 32 : 1],
+                                              f32x16 (&gb)[(MODE & 1) ? DB / 32 : 1], int lane) {
+  using C = BwdCfg<DA, DB, MODE>;
+  const int half = lane >> 5;
+  const u32x4* ta = stage;
+  const u32x4* tb = stage + C::BS * C::CA;
   // transpose-read addressing (see kl_common.hpp): row 4 * half + (lane % 16) / 4 of each
   // 16-row k-block, columns 16 * ((lane / 16) % 2) + 4 * (lane % 4) of each 32-column block.
   const int tr_row = 4 * half + ((lane & 15) >> 2);
@@ -141,6 +201,19 @@ __device__ __forceinline__ void bwd_tile(const u32x4* stage, const bf16x8 (&ra_o
       }
     }
   }
+}
+
+template <int DA, int DB, int MODE, bool MASK, typename StatsFn, typename OkFn>
+__device__ __forceinline__ void bwd_tile(const u32x4* stage, const bf16x8 (&ra_op)[DA / 16],
+                                         const bf16x8 (&rb_op)[DB / 16],
+                                         f32x16 (&ga)[(MODE & 2) ? DA / 32 : 1],
+                                         f32x16 (&gb)[(MODE & 1) ? DB / 32 : 1],
+                                         float ca, float cb, float sa, float sb, int lane,
+                                         StatsFn stats, OkFn ok) {
+  float dsa[16], dsb[16];
+  bwd_dlogits_tile<DA, DB, MODE, MASK>(stage, [&](int ks) { return ra_op[ks]; }, [&](int ks) { return rb_op[ks]; },
+                                       ca, cb, sa, sb, lane, stats, ok, dsa, dsb);
+  bwd_grad_tile<DA, DB, MODE>(stage, dsa, dsb, ga, gb, lane);
 }
 
 // Resident rows of this lane as MFMA B operands (zero rows past n).
@@ -185,7 +258,8 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   using C = BwdCfg<DA, DB, MODE>;
   __shared__ u32x4 smem[2 * C::STAGE];   // two-stage ring of key tiles
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+  // the wave index is uniform: in a scalar register, so are the values derived from it
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), half = lane >> 5;
   const int TQ = (NQ + C::BR - 1) / C::BR;
   const int logical = xcd_logical(blockIdx.x, gridDim.x);
   const int bh = logical / TQ;
@@ -208,6 +282,9 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   bf16x8 qa[DA / 16], qb[DB / 16];
   load_resident<DA>(qa, Qa, (size_t)bh * NQ, myq, NQ, half);
   load_resident<DB>(qb, Qb, (size_t)bh * NQ, myq, NQ, half);
+  // complete before the tile loop: a wait for them inside the loop would
+  // also wait for the loads of the next tile
+  wait_vmem();
 
   f32x16 dqa[C::WANT_A ? DA / 32 : 1], dqb[C::WANT_B ? DB / 32 : 1];
 #pragma unroll
@@ -220,7 +297,7 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   const TileDma<C::BS, C::CA, C::CB> dma(tid);
   const int kmax_ok = CAUSAL ? myq + off : NK;
 
-  auto tile = [&](const u32x4* stage, int kt) {
+  auto tile = [&](const u32x4* stage, int kt, int ln) {
     const int k0 = kt * C::BS;
     bool active = qw < NQ;
     bool need_mask = k0 + C::BS > NK;
@@ -234,19 +311,22 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
       const int k = k0 + 8 * (i >> 2) + 4 * half + (i & 3);
       return k < NK && k <= kmax_ok;
     };
-    if (need_mask)
-      bwd_tile<DA, DB, MODE, true>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, lane, stats, ok);
+    if (opaque(need_mask))
+      bwd_tile<DA, DB, MODE, true>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, ln, stats, ok);
     else
-      bwd_tile<DA, DB, MODE, false>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, lane, stats, ok);
+      bwd_tile<DA, DB, MODE, false>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, ln, stats, ok);
   };
 
+  // The transpose reads of a tile make the compiler wait for the next tile's
+  // loads (it cannot tell the two stages of the ring apart); by then, past the
+  // logit half of the tile, those loads have normally landed.
   if (ntiles > 0) dma.issue(rka, rkb, 0, smem, wave);
   wait_vmem();
   __syncthreads();
   for (int kt = 0; kt < ntiles; ++kt) {
     const int buf = kt & 1;
     if (kt + 1 < ntiles) dma.issue(rka, rkb, (kt + 1) * C::BS, smem + (buf ^ 1) * C::STAGE, wave);
-    tile(smem + buf * C::STAGE, kt);
+    tile(smem + buf * C::STAGE, kt, lane);
     wait_vmem();
     __syncthreads();
   }
@@ -268,10 +348,13 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
                  const float* __restrict__ lse_b, const float* __restrict__ g,
                  float* __restrict__ dKa, float* __restrict__ dKb) {
   using C = BwdCfg<DA, DB, MODE>;
-  __shared__ u32x4 smem[2 * C::STAGE];        // two-stage ring of query tiles
+  __shared__ u32x4 st0[C::STAGE];             // two stages of query tiles (two arrays: see the dQ kernel)
+  __shared__ u32x4 st1[C::STAGE];
   __shared__ f32x4 sstat[2][4][C::BS / 4];    // their row statistics: [stage][lsa2, lsb2, g, dl][rows / 4]
+  __shared__ float sraw[4][64];               // saved row values of the next tile, as loaded
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5;
+  // the wave index is uniform: in a scalar register, so are the values derived from it
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), half = lane >> 5;
   const int TK = (NK + C::BR - 1) / C::BR;
   const int logical = xcd_logical(blockIdx.x, gridDim.x);
   const int bh = logical / TK;
@@ -292,6 +375,9 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   bf16x8 ka[DA / 16], kb[DB / 16];
   load_resident<DA>(ka, Ka, (size_t)bh * NK, myk, NK, half);
   load_resident<DB>(kb, Kb, (size_t)bh * NK, myk, NK, half);
+  // complete before the tile loop: a wait for them inside the loop would
+  // also wait for the loads of the next tile
+  wait_vmem();
 
   f32x16 dka[C::WANT_A ? DA / 32 : 1], dkb[C::WANT_B ? DB / 32 : 1];
 #pragma unroll
@@ -303,20 +389,13 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   const rsrc_t rqb = make_rsrc(Qb + (size_t)bh * NQ * DB, (uint32_t)NQ * DB * 2u);
   const TileDma<C::BS, C::CA, C::CB> dma(tid);
 
-  // Row statistics of a streamed tile: threads 0..31 each prepare one row.
-  auto stats_stage = [&](int t, f32x4 (&dst)[4][C::BS / 4]) {
-    if (tid < C::BS) {
-      const int q = t * C::BS + tid;
-      const RowStats s = load_row_stats(kl, lse_a, lse_b, g, (size_t)bh * NQ + q, q < NQ);
-      float* p = reinterpret_cast<float*>(&dst[0][0]);
-      p[0 * C::BS + tid] = s.lsa2;
-      p[1 * C::BS + tid] = s.lsb2;
-      p[2 * C::BS + tid] = s.g;
-      p[3 * C::BS + tid] = s.dl;
-    }
+  const RowsDma rdma(kl, lse_a, lse_b, g, (size_t)bh * NQ, NQ);
+  auto stage_in = [&](int t, u32x4* dst) {
+    dma.issue(rqa, rqb, t * C::BS, dst, wave);
+    if (wave == 0) rdma.issue(t * C::BS, sraw, lane);
   };
 
-  auto tile = [&](const u32x4* stage, const f32x4 (&st)[4][C::BS / 4], int t) {
+  auto tile = [&](const u32x4* stage, const f32x4 (&st)[4][C::BS / 4], int t, int ln) {
     const int r0 = t * C::BS;
     bool active = kw < NK;
     bool need_mask = r0 + C::BS > NQ;
@@ -335,27 +414,29 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
       const int q = r0 + 8 * (i >> 2) + 4 * half + (i & 3);
       return q < NQ && (!CAUSAL || myk <= q + off);
     };
-    if (need_mask)
-      bwd_tile<DA, DB, MODE, true>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, lane, stats, ok);
+    if (opaque(need_mask))
+      bwd_tile<DA, DB, MODE, true>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, ln, stats, ok);
     else
-      bwd_tile<DA, DB, MODE, false>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, lane, stats, ok);
+      bwd_tile<DA, DB, MODE, false>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, ln, stats, ok);
   };
 
   if (t_begin < ntq) {
-    dma.issue(rqa, rqb, t_begin * C::BS, smem, wave);
-    stats_stage(t_begin, sstat[0]);
-  }
-  wait_vmem();
-  __syncthreads();
-  for (int t = t_begin; t < ntq; ++t) {
-    const int buf = (t - t_begin) & 1;
-    if (t + 1 < ntq) {
-      dma.issue(rqa, rqb, (t + 1) * C::BS, smem + (buf ^ 1) * C::STAGE, wave);
-      stats_stage(t + 1, sstat[buf ^ 1]);
-    }
-    tile(smem + buf * C::STAGE, sstat[buf], t);
+    stage_in(t_begin, st0);
     wait_vmem();
+    stage_row_stats<C::BS>(sraw, t_begin * C::BS, NQ, rdma.has_g, sstat[0], tid);
+  }
+  __syncthreads();
+  auto step = [&](const u32x4* cur, u32x4* nxt, int t, int buf) {
+    const bool has_next = t + 1 < ntq;
+    if (has_next) stage_in(t + 1, nxt);
+    tile(cur, sstat[buf], t, opaque(lane));
+    wait_vmem();
+    if (has_next) stage_row_stats<C::BS>(sraw, (t + 1) * C::BS, NQ, rdma.has_g, sstat[buf ^ 1], tid);
     __syncthreads();
+  };
+  for (int t = t_begin; t < ntq; t += 2) {
+    step(st0, st1, t, 0);
+    if (t + 1 < ntq) step(st1, st0, t + 1, 1);
   }
 
   if constexpr (C::WANT_B) write_grad<DB>(dKb, dkb, (size_t)bh * NK, kw, NK, sb, lane);

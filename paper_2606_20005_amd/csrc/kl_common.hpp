@@ -86,6 +86,13 @@ __device__ __forceinline__ bf16x4 lds_tr4(const u32x4* tile, int r, int e) {
   return __builtin_bit_cast(bf16x4, v);
 }
 
+// Transpose read at a byte offset of an LDS buffer with a layout of its own.
+__device__ __forceinline__ bf16x4 lds_tr4_at(const void* buf, int byte) {
+  const lds_char* base = (const lds_char*)(buf);
+  i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + byte));
+  return __builtin_bit_cast(bf16x4, v);
+}
+
 __device__ __forceinline__ bf16x8 cat8(const bf16x4& lo, const bf16x4& hi) {
   bf16x8 r;
 #pragma unroll
@@ -127,6 +134,32 @@ __device__ __forceinline__ void wait_vmem_le() {
 }
 __device__ __forceinline__ void wait_vmem() { wait_vmem_le<0>(); }
 
+// v, in a register the compiler cannot see through. Tile loops unrolled over
+// two stage arrays pass the lane index through this once per tile, so that
+// the compiler computes each copy's LDS addresses when it needs them rather
+// than all of them up front (holding them in registers); the stage bases
+// stay plain array addresses, which the compiler's alias tracking needs.
+__device__ __forceinline__ int opaque(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
+// fp32 atomic add to global memory, result unused (global_atomic_add_f32).
+// The pointer is cast to the global address space: through a generic pointer
+// the compiler would have to assume the add may write LDS and would wait for
+// it before every later LDS access.
+typedef __attribute__((address_space(1))) float global_float;
+__device__ __forceinline__ void atomic_add_global(float* p, float v) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  [[clang::atomic(no_remote_memory, no_fine_grained_memory, ignore_denormal_mode)]] {
+    __hip_atomic_fetch_add((global_float*)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+#endif
+}
+
+// s_waitcnt lgkmcnt(0) alone: this wave's LDS accesses have completed.
+__device__ __forceinline__ void wait_lds() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+
 // Workgroup barrier without a memory fence. __syncthreads() also releases and
 // acquires memory, which on gfx950 waits for every outstanding vector memory
 // operation of the wave, the tile loads still streaming into LDS included,
@@ -145,11 +178,13 @@ __device__ __forceinline__ void barrier_no_fence() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
+// CB = 0 stages rows of a single matrix.
 template <int R, int CA, int CB, int NT = kThreads>
 struct TileDma {
   static constexpr int NCH = R * (CA + CB) / NT;
   static constexpr int NCH_A = R * CA / NT;
   static_assert((R * (CA + CB)) % NT == 0 && (R * CA) % NT == 0, "staging split");
+  static_assert(CB == 0 || NCH > NCH_A, "second matrix");
   uint32_t voff[NCH];   // byte offset (from the tile's first row) of the chunk this lane fetches
 
   __device__ __forceinline__ explicit TileDma(int tid) {
@@ -159,7 +194,7 @@ struct TileDma {
       if (i < NCH_A) {
         const int r = p / CA, c = (p - r * CA) ^ swz<CA>(r);
         voff[i] = (uint32_t)(r * CA + c) * 16u;
-      } else {
+      } else if constexpr (CB > 0) {
         const int pp = p - R * CA;
         const int r = pp / CB, c = (pp - r * CB) ^ swz<CB>(r);
         voff[i] = (uint32_t)(r * CB + c) * 16u;

@@ -41,6 +41,17 @@ hipError_t launch_bwd_dq_m3(int da, int db, bool causal, const BwdArgs& a);
 hipError_t launch_bwd_dk_m1(int da, int db, bool causal, const BwdArgs& a);
 hipError_t launch_bwd_dk_m2(int da, int db, bool causal, const BwdArgs& a);
 hipError_t launch_bwd_dk_m3(int da, int db, bool causal, const BwdArgs& a);
+// Fused backward (Sec. 4.2): one key-owned kernel writes dK and adds dQ with
+// atomics; dQ must be zeroed first. bwd_fused_fits says whether the kernel
+// exists for these head dims and mode (its working set must fit in LDS).
+bool bwd_fused_fits(int da, int db, int mode);
+hipError_t launch_bwd_fused(int da, int db, bool causal, int mode, const BwdArgs& a);
+bool bwd_fused_fits_m1(int da, int db);
+bool bwd_fused_fits_m2(int da, int db);
+bool bwd_fused_fits_m3(int da, int db);
+hipError_t launch_bwd_fused_m1(int da, int db, bool causal, const BwdArgs& a);
+hipError_t launch_bwd_fused_m2(int da, int db, bool causal, const BwdArgs& a);
+hipError_t launch_bwd_fused_m3(int da, int db, bool causal, const BwdArgs& a);
 
 // Expands F(DA, DB) for every supported head-dim pair.
 #define STREAMKL_FOR_EACH_DIM_PAIR(F)                                        \

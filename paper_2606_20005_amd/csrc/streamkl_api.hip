@@ -33,6 +33,11 @@ int check_common(const void* Q1, const void* K1, const void* Q2, const void* K2,
   // one workgroup per 128 rows of one head; element offsets are 64-bit in the kernels
   if (bh * ((N_Q + 127LL) / 128) > kMaxGrid || bh * ((N_K + 127LL) / 128) > kMaxGrid)
     return STREAMKL_ERR_UNSUPPORTED;
+  // one (batch, head) slab of any tensor (bf16 inputs, fp32 gradients) is
+  // addressed with 32-bit byte offsets
+  const long long dmax = d1 > d2 ? d1 : d2;
+  if ((long long)N_Q * dmax * 4 > 0xffffffffLL || (long long)N_K * dmax * 4 > 0xffffffffLL)
+    return STREAMKL_ERR_UNSUPPORTED;
   *empty = bh == 0 || N_Q == 0;
   if (*empty) return STREAMKL_OK;
   if (!Q1 || !Q2) return STREAMKL_ERR_INVALID_ARG;
@@ -135,14 +140,49 @@ extern "C" int streamkl_fwd_split_count(int B, int H, int N_Q, int N_K, int d1, 
   return w < 1 ? 1 : (int)w;
 }
 
-extern "C" int streamkl_bwd(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H, int N_Q,
-                            int N_K, int d1, int d2, float s1, float s2, int causal, int direction,
-                            const float* kl, const float* lse1, const float* lse2, const float* dkl, float* dQ1,
-                            float* dK1, float* dQ2, float* dK2, hipStream_t stream) {
+namespace {
+
+// Gradient masks of the first- and second-slot distributions ("a", "b").
+struct BwdModes {
+  int q, k;   // bit 0: b, bit 1: a
+};
+
+BwdModes bwd_modes(bool rev, bool dq1, bool dk1, bool dq2, bool dk2) {
+  const bool dqa = rev ? dq2 : dq1, dqb = rev ? dq1 : dq2, dka = rev ? dk2 : dk1, dkb = rev ? dk1 : dk2;
+  return BwdModes{(dqb ? 1 : 0) | (dqa ? 2 : 0), (dkb ? 1 : 0) | (dka ? 2 : 0)};
+}
+
+// Adaptive strategy rule (Sec. 4.2) over 128-row tiles: fused when
+// T_Q * C <= T_K, C = 8, and in addition T_Q <= 4. Measured on MI355X
+// (16 heads, d = 128, N_K from 4K to 64K): the fused kernel is 1.5-10x faster
+// up to 512 query rows and slower from 1024 on, whatever N_K is, because its
+// per-pair cost (atomic adds, the shared dS tile) exceeds that of the
+// separate kernels once both have enough workgroups.
+constexpr long long kFusedRatio = 8;
+constexpr long long kFusedMaxQueryTiles = 4;
+
+bool fused_preferred(int N_Q, int N_K) {
+  const long long tq = (N_Q + 127LL) / 128, tk = (N_K + 127LL) / 128;
+  return tq * kFusedRatio <= tk && tq <= kFusedMaxQueryTiles;
+}
+
+int bwd_common(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H, int N_Q, int N_K,
+               int d1, int d2, float s1, float s2, int causal, int direction, const float* kl, const float* lse1,
+               const float* lse2, const float* dkl, float* dQ1, float* dK1, float* dQ2, float* dK2, int strategy,
+               hipStream_t stream) {
   if (!dQ1 && !dK1 && !dQ2 && !dK2) return STREAMKL_ERR_INVALID_ARG;
+  if (strategy != STREAMKL_BWD_AUTO && strategy != STREAMKL_BWD_SEPARATE && strategy != STREAMKL_BWD_FUSED)
+    return STREAMKL_ERR_INVALID_ARG;
   bool empty = false;
   int st = check_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, &empty);
   if (st != STREAMKL_OK) return st;
+  const bool rev = direction == STREAMKL_KL_REV;
+  const int da = rev ? d2 : d1, db = rev ? d1 : d2;
+  const BwdModes m = bwd_modes(rev, dQ1, dK1, dQ2, dK2);
+  const bool fused_ok = m.q != 0 && streamkl::bwd_fused_fits(da, db, m.q | m.k);
+  if (strategy == STREAMKL_BWD_FUSED && m.q != 0 && !fused_ok) return STREAMKL_ERR_UNSUPPORTED;
+  const bool fused = fused_ok && (strategy == STREAMKL_BWD_FUSED ||
+                                  (strategy == STREAMKL_BWD_AUTO && fused_preferred(N_Q, N_K)));
   const long long bh = (long long)B * H;
   // With N_Q = 0 every dK is zero and there is no dQ; with N_K = 0 every dQ is zero.
   if (bh == 0) return STREAMKL_OK;
@@ -157,7 +197,6 @@ extern "C" int streamkl_bwd(const void* Q1, const void* K1, const void* Q2, cons
   const void* ptrs[] = {kl, lse1, lse2, dkl, dQ1, dK1, dQ2, dK2};
   for (const void* p : ptrs)
     if (p && !aligned(p, 4)) return STREAMKL_ERR_INVALID_ARG;
-  const bool rev = direction == STREAMKL_KL_REV;
   BwdArgs a;
   a.Qa = static_cast<const uint16_t*>(rev ? Q2 : Q1);
   a.Ka = static_cast<const uint16_t*>(rev ? K2 : K1);
@@ -177,20 +216,53 @@ extern "C" int streamkl_bwd(const void* Q1, const void* K1, const void* Q2, cons
   a.dKa = rev ? dK2 : dK1;
   a.dKb = rev ? dK1 : dK2;
   a.stream = stream;
-  const int da = rev ? d2 : d1, db = rev ? d1 : d2;
-  const int mode_q = (a.dQb ? 1 : 0) | (a.dQa ? 2 : 0);
-  const int mode_k = (a.dKb ? 1 : 0) | (a.dKa ? 2 : 0);
   hipError_t e = hipSuccess;
-  if (mode_q) {
-    if (N_K == 0) {   // every row is empty: zero gradients
-      e = zero_fill(a.dQa, (size_t)bh * N_Q * da, stream);
-      if (e == hipSuccess) e = zero_fill(a.dQb, (size_t)bh * N_Q * db, stream);
-    } else {
-      e = streamkl::launch_bwd_dq(da, db, causal == 1, mode_q, a);
-    }
+  if (m.q && N_K == 0) {   // every row is empty: zero gradients
+    e = zero_fill(a.dQa, (size_t)bh * N_Q * da, stream);
+    if (e == hipSuccess) e = zero_fill(a.dQb, (size_t)bh * N_Q * db, stream);
+    return hip_status(e);
   }
-  if (e == hipSuccess && mode_k && N_K > 0) e = streamkl::launch_bwd_dk(da, db, causal == 1, mode_k, a);
+  if (fused) {
+    // dQ accumulates atomically over key blocks: start from zero
+    e = zero_fill(a.dQa, (size_t)bh * N_Q * da, stream);
+    if (e == hipSuccess) e = zero_fill(a.dQb, (size_t)bh * N_Q * db, stream);
+    if (e == hipSuccess) e = streamkl::launch_bwd_fused(da, db, causal == 1, m.q | m.k, a);
+    return hip_status(e);
+  }
+  if (m.q) e = streamkl::launch_bwd_dq(da, db, causal == 1, m.q, a);
+  if (e == hipSuccess && m.k && N_K > 0) e = streamkl::launch_bwd_dk(da, db, causal == 1, m.k, a);
   return hip_status(e);
+}
+
+}  // namespace
+
+extern "C" int streamkl_bwd(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H, int N_Q,
+                            int N_K, int d1, int d2, float s1, float s2, int causal, int direction,
+                            const float* kl, const float* lse1, const float* lse2, const float* dkl, float* dQ1,
+                            float* dK1, float* dQ2, float* dK2, hipStream_t stream) {
+  return bwd_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, kl, lse1, lse2, dkl, dQ1,
+                    dK1, dQ2, dK2, STREAMKL_BWD_SEPARATE, stream);
+}
+
+extern "C" int streamkl_bwd_ex(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H,
+                               int N_Q, int N_K, int d1, int d2, float s1, float s2, int causal, int direction,
+                               const float* kl, const float* lse1, const float* lse2, const float* dkl,
+                               float* dQ1, float* dK1, float* dQ2, float* dK2, int strategy, hipStream_t stream) {
+  return bwd_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, kl, lse1, lse2, dkl, dQ1,
+                    dK1, dQ2, dK2, strategy, stream);
+}
+
+extern "C" int streamkl_bwd_choose(int B, int H, int N_Q, int N_K, int d1, int d2, int causal, int direction,
+                                   int grads) {
+  if (B < 0 || H < 0 || N_Q < 0 || N_K < 0) return 0;
+  if (causal != 0 && causal != 1) return 0;
+  if (direction != STREAMKL_KL_FWD && direction != STREAMKL_KL_REV) return 0;
+  if (!supported_dim(d1) || !supported_dim(d2) || grads <= 0 || grads > 15) return 0;
+  const bool rev = direction == STREAMKL_KL_REV;
+  const BwdModes m = bwd_modes(rev, grads & STREAMKL_GRAD_DQ1, grads & STREAMKL_GRAD_DK1, grads & STREAMKL_GRAD_DQ2,
+                               grads & STREAMKL_GRAD_DK2);
+  const bool fused_ok = m.q != 0 && streamkl::bwd_fused_fits(rev ? d2 : d1, rev ? d1 : d2, m.q | m.k);
+  return fused_ok && fused_preferred(N_Q, N_K) ? STREAMKL_BWD_FUSED : STREAMKL_BWD_SEPARATE;
 }
 
 extern "C" const char* streamkl_strerror(int status) {
@@ -214,6 +286,24 @@ hipError_t launch_bwd_dq(int da, int db, bool causal, int mode, const BwdArgs& a
     case 1: return launch_bwd_dq_m1(da, db, causal, a);
     case 2: return launch_bwd_dq_m2(da, db, causal, a);
     case 3: return launch_bwd_dq_m3(da, db, causal, a);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+bool bwd_fused_fits(int da, int db, int mode) {
+  switch (mode) {
+    case 1: return bwd_fused_fits_m1(da, db);
+    case 2: return bwd_fused_fits_m2(da, db);
+    case 3: return bwd_fused_fits_m3(da, db);
+    default: return false;
+  }
+}
+
+hipError_t launch_bwd_fused(int da, int db, bool causal, int mode, const BwdArgs& a) {
+  switch (mode) {
+    case 1: return launch_bwd_fused_m1(da, db, causal, a);
+    case 2: return launch_bwd_fused_m2(da, db, causal, a);
+    case 3: return launch_bwd_fused_m3(da, db, causal, a);
     default: return hipErrorInvalidValue;
   }
 }

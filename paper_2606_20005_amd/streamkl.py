@@ -7,7 +7,7 @@ not been built; there is no fallback implementation.
 
     kl, lse1, lse2 = fwd(q1, k1, q2, k2, s1, s2, causal, direction)
     kl, lse1, lse2 = fwd_split(q1, k1, q2, k2, s1, s2, causal, direction, splits="auto")
-    dQ1, dK1, dQ2, dK2 = bwd(q1, k1, q2, k2, kl, lse1, lse2, dkl, ..., want=("dq2", "dk2"))
+    dQ1, dK1, dQ2, dK2 = bwd(q1, k1, q2, k2, kl, lse1, lse2, dkl, ..., want=("dq2", "dk2"), strategy="auto")
     loss = attention_kl(q1, k1, q2, k2, causal=True).mean(); loss.backward()
 """
 from __future__ import annotations
@@ -22,9 +22,11 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libstreamkl
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP = 0, 1, 2, 3
 FWD, REV = 0, 1
-ENTRY_POINTS = ("streamkl_fwd", "streamkl_bwd", "streamkl_fwd_split", "streamkl_fwd_split_workspace_bytes",
-                "streamkl_fwd_split_count", "streamkl_strerror", "streamkl_version",
-                "streamkl_supported_head_dim")
+BWD_AUTO, BWD_SEPARATE, BWD_FUSED = 0, 1, 2
+GRAD_BITS = {"dq1": 1, "dk1": 2, "dq2": 4, "dk2": 8}
+ENTRY_POINTS = ("streamkl_fwd", "streamkl_bwd", "streamkl_bwd_ex", "streamkl_bwd_choose", "streamkl_fwd_split",
+                "streamkl_fwd_split_workspace_bytes", "streamkl_fwd_split_count", "streamkl_strerror",
+                "streamkl_version", "streamkl_supported_head_dim")
 
 
 def _load():
@@ -37,6 +39,11 @@ def _load():
     lib.streamkl_fwd.restype = i
     lib.streamkl_bwd.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, f, f, i, i, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.streamkl_bwd.restype = i
+    lib.streamkl_bwd_ex.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, f, f, i, i, vp, vp, vp, vp, vp, vp, vp, vp, i,
+                                    vp]
+    lib.streamkl_bwd_ex.restype = i
+    lib.streamkl_bwd_choose.argtypes = [i, i, i, i, i, i, i, i, i]
+    lib.streamkl_bwd_choose.restype = i
     sz = ctypes.c_size_t
     lib.streamkl_fwd_split.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, f, f, i, i, i, vp, sz, vp, vp, vp, vp]
     lib.streamkl_fwd_split.restype = i
@@ -174,13 +181,36 @@ def fwd_split(q1, k1, q2, k2, s1=None, s2=None, causal=False, direction=FWD, spl
     return kl, lse1, lse2
 
 
+_STRATEGIES = {"auto": BWD_AUTO, "separate": BWD_SEPARATE, "fused": BWD_FUSED}
+
+
+def _strategy(strategy) -> int:
+    if isinstance(strategy, str):
+        if strategy not in _STRATEGIES:
+            raise ValueError(f"strategy must be one of {sorted(_STRATEGIES)}, got {strategy!r}")
+        return _STRATEGIES[strategy]
+    return int(strategy)
+
+
+def bwd_choose(B, H, n_q, n_k, d1, d2, causal=False, direction=FWD, want=("dq2", "dk2")) -> str:
+    """streamkl_bwd_choose: the strategy ("separate" or "fused") the adaptive rule picks."""
+    bits = 0
+    for n in want:
+        bits |= GRAD_BITS[n]
+    r = lib.streamkl_bwd_choose(B, H, n_q, n_k, d1, d2, int(bool(causal)), _direction(direction), bits)
+    if r == 0:
+        raise StreamKLError(ERR_INVALID_ARG, "streamkl_bwd_choose")
+    return "fused" if r == BWD_FUSED else "separate"
+
+
 def bwd(q1, k1, q2, k2, kl, lse1, lse2, dkl=None, s1=None, s2=None, causal=False, direction=FWD,
-        want=("dq2", "dk2"), out=None):
-    """streamkl_bwd: returns (dQ1, dK1, dQ2, dK2), float32, None where not requested.
+        want=("dq2", "dk2"), out=None, strategy="separate"):
+    """streamkl_bwd / streamkl_bwd_ex: returns (dQ1, dK1, dQ2, dK2), float32, None where not requested.
 
     want: any of "dq1", "dk1", "dq2", "dk2". dkl: per-row upstream gradient
     (float32 [B, H, N_Q]) or None for all ones. ``out`` may map those names to
-    preallocated tensors.
+    preallocated tensors. strategy: "separate" (streamkl_bwd, reproducible),
+    "fused" (one kernel, dQ by atomics) or "auto" (the adaptive rule).
     """
     B, H, NQ, NK, d1, d2 = _check_inputs(q1, k1, q2, k2)
     s1, s2 = _scales(s1, s2, d1, d2)
@@ -201,48 +231,57 @@ def bwd(q1, k1, q2, k2, kl, lse1, lse2, dkl=None, s1=None, s2=None, causal=False
                 torch.empty(shapes[n], dtype=torch.float32, device=dev)
         else:
             grads[n] = None
+    strat = _strategy(strategy)
+    args = (_p(q1), _p(k1), _p(q2), _p(k2), B, H, NQ, NK, d1, d2, s1, s2, int(bool(causal)), _direction(direction),
+            _p(kl), _p(lse1), _p(lse2), _p(dkl), _p(grads["dq1"]), _p(grads["dk1"]), _p(grads["dq2"]),
+            _p(grads["dk2"]))
     with torch.cuda.device(dev):
-        st = lib.streamkl_bwd(_p(q1), _p(k1), _p(q2), _p(k2), B, H, NQ, NK, d1, d2, s1, s2,
-                              int(bool(causal)), _direction(direction), _p(kl), _p(lse1), _p(lse2), _p(dkl),
-                              _p(grads["dq1"]), _p(grads["dk1"]), _p(grads["dq2"]), _p(grads["dk2"]),
-                              _stream(dev))
+        if strat == BWD_SEPARATE:
+            st, where = lib.streamkl_bwd(*args, _stream(dev)), "streamkl_bwd"
+        else:
+            st, where = lib.streamkl_bwd_ex(*args, strat, _stream(dev)), "streamkl_bwd_ex"
     if st != OK:
-        raise StreamKLError(st, "streamkl_bwd")
+        raise StreamKLError(st, where)
     return grads["dq1"], grads["dk1"], grads["dq2"], grads["dk2"]
 
 
 class _AttentionKL(torch.autograd.Function):
     @staticmethod
-    def forward(ctx, q1, k1, q2, k2, s1, s2, causal, direction):
+    def forward(ctx, q1, k1, q2, k2, s1, s2, causal, direction, bwd_strategy):
         # the adaptive split count is 1 (the single-pass kernel) unless the heads have few query rows
         kl, lse1, lse2 = fwd_split(q1, k1, q2, k2, s1, s2, causal, direction, splits="auto")
         ctx.save_for_backward(q1, k1, q2, k2, kl, lse1, lse2)
-        ctx.cfg = (s1, s2, causal, direction)
+        ctx.cfg = (s1, s2, causal, direction, bwd_strategy)
         ctx.mark_non_differentiable(lse1, lse2)
         return kl, lse1, lse2
 
     @staticmethod
     def backward(ctx, gkl, _glse1, _glse2):
         q1, k1, q2, k2, kl, lse1, lse2 = ctx.saved_tensors
-        s1, s2, causal, direction = ctx.cfg
+        s1, s2, causal, direction, strategy = ctx.cfg
         names = [n for n, need in zip(("dq1", "dk1", "dq2", "dk2"), ctx.needs_input_grad[:4]) if need]
         if not names:
-            return (None,) * 8
+            return (None,) * 9
         g = gkl.to(torch.float32).contiguous()
-        dq1, dk1, dq2, dk2 = bwd(q1, k1, q2, k2, kl, lse1, lse2, g, s1, s2, causal, direction, want=names)
+        dq1, dk1, dq2, dk2 = bwd(q1, k1, q2, k2, kl, lse1, lse2, g, s1, s2, causal, direction, want=names,
+                                 strategy=strategy)
         cast = lambda t, ref: None if t is None else t.to(ref.dtype)   # noqa: E731
-        return cast(dq1, q1), cast(dk1, k1), cast(dq2, q2), cast(dk2, k2), None, None, None, None
+        return cast(dq1, q1), cast(dk1, k1), cast(dq2, q2), cast(dk2, k2), None, None, None, None, None
 
 
-def attention_kl(q1, k1, q2, k2, *, s1=None, s2=None, causal=False, direction="fwd", return_lse=False):
+def attention_kl(q1, k1, q2, k2, *, s1=None, s2=None, causal=False, direction="fwd", return_lse=False,
+                 bwd_strategy="auto"):
     """Per-row KL between softmax(s1 q1 k1^T) and softmax(s2 q2 k2^T), differentiable.
 
     Returns kl [B, H, N_Q] (and lse1, lse2 if ``return_lse``). The paper's
     training objective is ``attention_kl(...).mean()``. Gradients flow to the
     inputs that require them: (q2, k2) in standard distillation (Setting 1),
     (q1, k1) when the first distribution is trained (Setting 2), or both.
+    bwd_strategy: "auto" (the adaptive rule of streamkl_bwd_choose), "fused"
+    or "separate" (bitwise reproducible gradients).
     """
     d1, d2 = q1.shape[-1], q2.shape[-1]
     s1, s2 = _scales(s1, s2, d1, d2)
-    kl, lse1, lse2 = _AttentionKL.apply(q1, k1, q2, k2, s1, s2, bool(causal), _direction(direction))
+    _strategy(bwd_strategy)
+    kl, lse1, lse2 = _AttentionKL.apply(q1, k1, q2, k2, s1, s2, bool(causal), _direction(direction), bwd_strategy)
     return (kl, lse1, lse2) if return_lse else kl

@@ -81,6 +81,67 @@ def test_argument_checks(sk, call, kw, expect):
     assert call(sk, **kw) == expect
 
 
+def bwd_ex_call(sk, strategy=0, **kw):
+    a = dict(Q1=FAKE, K1=FAKE, Q2=FAKE, K2=FAKE, B=1, H=2, NQ=64, NK=64, d1=64, d2=64, s1=0.125, s2=0.125,
+             causal=0, direction=0, kl=FAKE, lse1=FAKE, lse2=FAKE, dkl=None, dQ1=None, dK1=None, dQ2=FAKE,
+             dK2=FAKE, stream=None)
+    a.update(kw)
+    return sk.lib.streamkl_bwd_ex(a["Q1"], a["K1"], a["Q2"], a["K2"], a["B"], a["H"], a["NQ"], a["NK"], a["d1"],
+                                  a["d2"], a["s1"], a["s2"], a["causal"], a["direction"], a["kl"], a["lse1"],
+                                  a["lse2"], a["dkl"], a["dQ1"], a["dK1"], a["dQ2"], a["dK2"], strategy, a["stream"])
+
+
+@pytest.mark.parametrize("strategy", [0, 1, 2])
+@pytest.mark.parametrize("kw,expect", [
+    (dict(Q1=None), 1), (dict(kl=None), 1), (dict(NK=-1), 1), (dict(causal=2), 1), (dict(s2=0.0), 1),
+    (dict(K2=MIS), 1), (dict(dQ2=ctypes.c_void_p(0x100002)), 1), (dict(dQ2=None, dK2=None), 1),
+    (dict(d1=96), 2), (dict(B=0), 0), (dict(NK=5_000_000, d1=256), 2),
+])
+def test_bwd_ex_argument_checks(sk, strategy, kw, expect):
+    assert bwd_ex_call(sk, strategy, **kw) == expect
+
+
+def test_bwd_ex_rejects_unknown_strategy(sk):
+    assert bwd_ex_call(sk, 3) == 1
+    assert bwd_ex_call(sk, -1) == 1
+
+
+def test_bwd_ex_fused_needs_lds_room(sk):
+    # all four gradients at d1 = d2 = 256: the fused kernel's LDS working set
+    # exceeds 160 KiB, so the explicit request is unsupported (nothing launched)
+    four = dict(d1=256, d2=256, dQ1=FAKE, dK1=FAKE, dQ2=FAKE, dK2=FAKE)
+    assert bwd_ex_call(sk, 2, **four) == 2
+
+
+def test_extent_limit_of_32_bit_slabs(sk):
+    # N * max(d) * 4 must stay below 2^32 bytes per head
+    assert fwd_call(sk, NK=4_194_304, d1=256) == 2
+    assert bwd_call(sk, NQ=4_194_304, d2=256) == 2
+    assert fwd_call(sk, NQ=0, NK=4_194_303, d1=256, Q1=None, Q2=None) == 0
+
+
+def test_bwd_choose_follows_the_adaptive_rule(sk):
+    """Fused when T_Q * 8 <= T_K and T_Q <= 4 (128-row tiles), the fused kernel
+    exists for the request, and some dQ is requested."""
+    assert sk.bwd_choose(16, 1, 16, 65536, 128, 128) == "fused"       # decode: T_Q = 1, T_K = 512
+    assert sk.bwd_choose(1, 32, 16384, 16384, 128, 128) == "separate"  # T_Q = T_K = 128
+    assert sk.bwd_choose(1, 8, 8192, 131072, 192, 64, True) == "separate"  # T_Q = 64 > 4
+    assert sk.bwd_choose(1, 1, 512, 4096, 64, 64) == "fused"          # 4 * 8 <= 32 (boundary)
+    assert sk.bwd_choose(1, 1, 512, 3968, 64, 64) == "separate"       # 4 * 8 > 31
+    assert sk.bwd_choose(1, 1, 513, 1 << 20, 64, 64) == "separate"    # T_Q = 5 > 4
+    assert sk.bwd_choose(1, 1, 16, 65536, 64, 64, want=("dk2",)) == "separate"   # no dQ: dK kernel only
+    assert sk.bwd_choose(1, 1, 16, 65536, 256, 256, want=("dq1", "dk1", "dq2", "dk2")) == "separate"
+    assert sk.bwd_choose(1, 1, 16, 65536, 128, 128, want=("dq1", "dk1", "dq2", "dk2")) == "fused"
+    for bad in (dict(B=-1), dict(n_k=-5), dict(d1=96), dict(want=())):
+        a = dict(B=1, H=1, n_q=16, n_k=4096, d1=64, d2=64, causal=False, direction=0, want=("dq2", "dk2"))
+        a.update(bad)
+        with pytest.raises(sk.StreamKLError):
+            sk.bwd_choose(**a)
+    assert sk.lib.streamkl_bwd_choose(1, 1, 16, 4096, 64, 64, 2, 0, 12) == 0    # causal flag
+    assert sk.lib.streamkl_bwd_choose(1, 1, 16, 4096, 64, 64, 0, 2, 12) == 0    # direction
+    assert sk.lib.streamkl_bwd_choose(1, 1, 16, 4096, 64, 64, 0, 0, 16) == 0    # unknown gradient bit
+
+
 def test_bwd_needs_one_gradient(sk):
     assert bwd_call(sk, dQ2=None, dK2=None) == 1
 
