@@ -164,6 +164,46 @@ __device__ __forceinline__ void bwd_dlogits_tile(const u32x4* stage, OpA ra_op, 
   }
 }
 
+// Byte offsets within a stage of the transpose reads of the gradient
+// contraction, for the calling lane: [32-column block nb][rows tr_row, tr_row
+// + 8 of the first 16-row k-block]. The second k-block is 16 rows further,
+// which the swizzle (a function of the row modulo 16) turns into a constant
+// offset. They are computed once per kernel and passed through opaque(): the
+// tile loops then address each stage as its array base plus these registers,
+// with no per-tile address arithmetic, and the compiler still sees which
+// stage array every read touches (it would otherwise wait for the loads in
+// flight into the other stage before each read).
+template <int DA, int DB, int MODE>
+struct TrOffsets {
+  using C = BwdCfg<DA, DB, MODE>;
+  int a[C::WANT_A ? DA / 32 : 1][2];
+  int b[C::WANT_B ? DB / 32 : 1][2];
+  __device__ __forceinline__ explicit TrOffsets(int lane) {
+    const int half = lane >> 5;
+    // transpose-read addressing (see kl_common.hpp): row 4 * half + (lane % 16) / 4 of each
+    // 16-row k-block, columns 16 * ((lane / 16) % 2) + 4 * (lane % 4) of each 32-column block.
+    const int tr_row = 4 * half + ((lane & 15) >> 2);
+    const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if constexpr (C::WANT_A) {
+#pragma unroll
+        for (int nb = 0; nb < DA / 32; ++nb) {
+          const int e = 32 * nb + tr_col;
+          a[nb][h] = opaque(chunk_slot<C::CA>(tr_row + 8 * h, e >> 3) * 16 + ((e >> 2) & 1) * 8);
+        }
+      }
+      if constexpr (C::WANT_B) {
+#pragma unroll
+        for (int nb = 0; nb < DB / 32; ++nb) {
+          const int e = 32 * nb + tr_col;
+          b[nb][h] = opaque(C::BS * C::CA * 16 + chunk_slot<C::CB>(tr_row + 8 * h, e >> 3) * 16 + ((e >> 2) & 1) * 8);
+        }
+      }
+    }
+  }
+};
+
 // Gradient tiles of the resident rows from the logit gradients of one tile:
 //   grad[resident][d] += sum_streamed dS[streamed][resident] * X[streamed][d]
 // with X the streamed rows of the stage (transpose reads). dS, rounded to
@@ -171,23 +211,17 @@ __device__ __forceinline__ void bwd_dlogits_tile(const u32x4* stage, OpA ra_op, 
 template <int DA, int DB, int MODE>
 __device__ __forceinline__ void bwd_grad_tile(const u32x4* stage, const float (&dsa)[16], const float (&dsb)[16],
                                               f32x16 (&ga)[(MODE & 2) ? DA / 32 : 1],
-                                              f32x16 (&gb)[(MODE & 1) ? DB / 32 : 1], int lane) {
+                                              f32x16 (&gb)[(MODE & 1) ? DB / 32 : 1],
+                                              const TrOffsets<DA, DB, MODE>& to) {
   using C = BwdCfg<DA, DB, MODE>;
-  const int half = lane >> 5;
-  const u32x4* ta = stage;
-  const u32x4* tb = stage + C::BS * C::CA;
-  // transpose-read addressing (see kl_common.hpp): row 4 * half + (lane % 16) / 4 of each
-  // 16-row k-block, columns 16 * ((lane / 16) % 2) + 4 * (lane % 4) of each 32-column block.
-  const int tr_row = 4 * half + ((lane & 15) >> 2);
-  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
     if constexpr (C::WANT_B) {
       const bf16x8 aop = pack8(dsb + 8 * s);
 #pragma unroll
       for (int nb = 0; nb < DB / 32; ++nb) {
-        const bf16x8 bop = cat8(lds_tr4<C::CB>(tb, 16 * s + tr_row, 32 * nb + tr_col),
-                                lds_tr4<C::CB>(tb, 16 * s + 8 + tr_row, 32 * nb + tr_col));
+        const bf16x8 bop = cat8(lds_tr4_at(stage, to.b[nb][0] + 256 * C::CB * s),
+                                lds_tr4_at(stage, to.b[nb][1] + 256 * C::CB * s));
         gb[nb] = mfma32(aop, bop, gb[nb]);
       }
     }
@@ -195,8 +229,8 @@ __device__ __forceinline__ void bwd_grad_tile(const u32x4* stage, const float (&
       const bf16x8 aop = pack8(dsa + 8 * s);
 #pragma unroll
       for (int nb = 0; nb < DA / 32; ++nb) {
-        const bf16x8 bop = cat8(lds_tr4<C::CA>(ta, 16 * s + tr_row, 32 * nb + tr_col),
-                                lds_tr4<C::CA>(ta, 16 * s + 8 + tr_row, 32 * nb + tr_col));
+        const bf16x8 bop = cat8(lds_tr4_at(stage, to.a[nb][0] + 256 * C::CA * s),
+                                lds_tr4_at(stage, to.a[nb][1] + 256 * C::CA * s));
         ga[nb] = mfma32(aop, bop, ga[nb]);
       }
     }
@@ -209,11 +243,11 @@ __device__ __forceinline__ void bwd_tile(const u32x4* stage, const bf16x8 (&ra_o
                                          f32x16 (&ga)[(MODE & 2) ? DA / 32 : 1],
                                          f32x16 (&gb)[(MODE & 1) ? DB / 32 : 1],
                                          float ca, float cb, float sa, float sb, int lane,
-                                         StatsFn stats, OkFn ok) {
+                                         StatsFn stats, OkFn ok, const TrOffsets<DA, DB, MODE>& to) {
   float dsa[16], dsb[16];
   bwd_dlogits_tile<DA, DB, MODE, MASK>(stage, [&](int ks) { return ra_op[ks]; }, [&](int ks) { return rb_op[ks]; },
                                        ca, cb, sa, sb, lane, stats, ok, dsa, dsb);
-  bwd_grad_tile<DA, DB, MODE>(stage, dsa, dsb, ga, gb, lane);
+  bwd_grad_tile<DA, DB, MODE>(stage, dsa, dsb, ga, gb, to);
 }
 
 // Resident rows of this lane as MFMA B operands (zero rows past n).
@@ -256,7 +290,11 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
                  const float* __restrict__ lse_b, const float* __restrict__ g,
                  float* __restrict__ dQa, float* __restrict__ dQb) {
   using C = BwdCfg<DA, DB, MODE>;
-  __shared__ u32x4 smem[2 * C::STAGE];   // two-stage ring of key tiles
+  // Two stages of key tiles as two arrays, so that the compiler can tell
+  // which stage each LDS read touches (the loop names each stage's array
+  // explicitly, two tiles per trip).
+  __shared__ u32x4 st0[C::STAGE];
+  __shared__ u32x4 st1[C::STAGE];
 
   // the wave index is uniform: in a scalar register, so are the values derived from it
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), half = lane >> 5;
@@ -297,7 +335,8 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   const TileDma<C::BS, C::CA, C::CB> dma(tid);
   const int kmax_ok = CAUSAL ? myq + off : NK;
 
-  auto tile = [&](const u32x4* stage, int kt, int ln) {
+  const TrOffsets<DA, DB, MODE> tro(lane);
+  auto tile = [&](const u32x4* stage, int kt) {
     const int k0 = kt * C::BS;
     bool active = qw < NQ;
     bool need_mask = k0 + C::BS > NK;
@@ -312,23 +351,23 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
       return k < NK && k <= kmax_ok;
     };
     if (opaque(need_mask))
-      bwd_tile<DA, DB, MODE, true>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, ln, stats, ok);
+      bwd_tile<DA, DB, MODE, true>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, lane, stats, ok, tro);
     else
-      bwd_tile<DA, DB, MODE, false>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, ln, stats, ok);
+      bwd_tile<DA, DB, MODE, false>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, lane, stats, ok, tro);
   };
 
-  // The transpose reads of a tile make the compiler wait for the next tile's
-  // loads (it cannot tell the two stages of the ring apart); by then, past the
-  // logit half of the tile, those loads have normally landed.
-  if (ntiles > 0) dma.issue(rka, rkb, 0, smem, wave);
+  if (ntiles > 0) dma.issue(rka, rkb, 0, st0, wave);
   wait_vmem();
   __syncthreads();
-  for (int kt = 0; kt < ntiles; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < ntiles) dma.issue(rka, rkb, (kt + 1) * C::BS, smem + (buf ^ 1) * C::STAGE, wave);
-    tile(smem + buf * C::STAGE, kt, lane);
+  auto step = [&](const u32x4* cur, u32x4* nxt, int kt) {
+    if (kt + 1 < ntiles) dma.issue(rka, rkb, (kt + 1) * C::BS, nxt, wave);
+    tile(cur, kt);
     wait_vmem();
     __syncthreads();
+  };
+  for (int kt = 0; kt < ntiles; kt += 2) {
+    step(st0, st1, kt);
+    if (kt + 1 < ntiles) step(st1, st0, kt + 1);
   }
 
   if constexpr (C::WANT_B) write_grad<DB>(dQb, dqb, (size_t)bh * NQ, qw, NQ, sb, lane);
@@ -395,7 +434,8 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
     if (wave == 0) rdma.issue(t * C::BS, sraw, lane);
   };
 
-  auto tile = [&](const u32x4* stage, const f32x4 (&st)[4][C::BS / 4], int t, int ln) {
+  const TrOffsets<DA, DB, MODE> tro(lane);
+  auto tile = [&](const u32x4* stage, const f32x4 (&st)[4][C::BS / 4], int t) {
     const int r0 = t * C::BS;
     bool active = kw < NK;
     bool need_mask = r0 + C::BS > NQ;
@@ -415,9 +455,9 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
       return q < NQ && (!CAUSAL || myk <= q + off);
     };
     if (opaque(need_mask))
-      bwd_tile<DA, DB, MODE, true>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, ln, stats, ok);
+      bwd_tile<DA, DB, MODE, true>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, lane, stats, ok, tro);
     else
-      bwd_tile<DA, DB, MODE, false>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, ln, stats, ok);
+      bwd_tile<DA, DB, MODE, false>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, lane, stats, ok, tro);
   };
 
   if (t_begin < ntq) {
@@ -429,7 +469,7 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   auto step = [&](const u32x4* cur, u32x4* nxt, int t, int buf) {
     const bool has_next = t + 1 < ntq;
     if (has_next) stage_in(t + 1, nxt);
-    tile(cur, sstat[buf], t, opaque(lane));
+    tile(cur, sstat[buf], t);
     wait_vmem();
     if (has_next) stage_row_stats<C::BS>(sraw, (t + 1) * C::BS, NQ, rdma.has_g, sstat[buf ^ 1], tid);
     __syncthreads();

@@ -79,8 +79,9 @@ __device__ __forceinline__ void store_ds(u32x4* tile, int k, int half, const flo
   }
 }
 
-// dQ contribution of one 32-column block: sum over the key block's 16-key
-// groups j < jend (of NJ) of dS[q][keys] . K[keys][32 cb ..].
+// Per-lane byte offsets of the transpose reads of the dQ contraction for
+// 32-column block cb (see dq_block_mma), computed once per kernel and passed
+// through opaque() for the reason given at TrOffsets.
 //
 // A operand (dS, query row lane % 32): two transpose reads of four key rows
 // each, keys 16 j + 8 half + 4 rho + 0..3, unit u = 4 g + lane % 4. In the dS
@@ -89,26 +90,38 @@ __device__ __forceinline__ void store_ds(u32x4* tile, int k, int half, const flo
 // B operand (K, column 32 cb + lane % 32): the same key rows of the key block
 // copy; its swizzle depends only on the row modulo 16, so the address is a
 // per-lane base per rho plus 16 j rows. All group offsets are immediates.
-template <int CPR, int NJ>
-__device__ __forceinline__ f32x16 dq_block_mma(const u32x4* ds_tile, const u32x4* kres, int cb, int jend, int lane) {
+struct DqOffsets {
+  int a[2][2];   // [rho][j % 2]
+  int b[2];      // [rho]
+};
+
+template <int CPR>
+__device__ __forceinline__ DqOffsets dq_offsets(int lane, int cb) {
+  DqOffsets o;
   const int half = lane >> 5, g = (lane >> 4) & 1, jj = lane & 15;
   const int u = 4 * g + (jj & 3);
   const int col = 32 * cb + 16 * g + 4 * (jj & 3);
-  int a_base[2][2], b_base[2];
 #pragma unroll
   for (int rho = 0; rho < 2; ++rho) {
     const int kr = 8 * half + 4 * rho + (jj >> 2);   // key row of group 0
 #pragma unroll
-    for (int par = 0; par < 2; ++par) a_base[rho][par] = ds_unit_byte(kr + 16 * par, u) - 1024 * par;
-    b_base[rho] = chunk_slot<CPR>(kr, col >> 3) * 16 + ((col >> 2) & 1) * 8;
+    for (int par = 0; par < 2; ++par) o.a[rho][par] = opaque(ds_unit_byte(kr + 16 * par, u) - 1024 * par);
+    o.b[rho] = opaque(chunk_slot<CPR>(kr, col >> 3) * 16 + ((col >> 2) & 1) * 8);
   }
+  return o;
+}
+
+// dQ contribution of one 32-column block: sum over the key block's 16-key
+// groups j < jend (of NJ) of dS[q][keys] . K[keys][32 cb ..].
+template <int CPR, int NJ>
+__device__ __forceinline__ f32x16 dq_block_mma(const u32x4* ds_tile, const u32x4* kres, const DqOffsets& o,
+                                               int jend) {
   f32x16 acc = zero16();
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
     if (j < jend) {
-      const bf16x8 aop = cat8(lds_tr4_at(ds_tile, a_base[0][j & 1] + 1024 * j),
-                              lds_tr4_at(ds_tile, a_base[1][j & 1] + 1024 * j));
-      const bf16x8 bop = cat8(lds_tr4_at(kres, b_base[0] + 256 * CPR * j), lds_tr4_at(kres, b_base[1] + 256 * CPR * j));
+      const bf16x8 aop = cat8(lds_tr4_at(ds_tile, o.a[0][j & 1] + 1024 * j), lds_tr4_at(ds_tile, o.a[1][j & 1] + 1024 * j));
+      const bf16x8 bop = cat8(lds_tr4_at(kres, o.b[0] + 256 * CPR * j), lds_tr4_at(kres, o.b[1] + 256 * CPR * j));
       acc = mfma32(aop, bop, acc);
     }
   }
@@ -234,6 +247,7 @@ kl_bwd_fused_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict_
     const int k = i + rot;
     return t_begin + (k < nt ? k : k - nt);
   };
+  const TrOffsets<DA, DB, MODE> tro(lane);
   auto stage_in = [&](int t, u32x4* dst) {
     dma.issue(rqa, rqb, t * C::BS, dst, wave);
     if (wave == 0) rdma.issue(t * C::BS, reinterpret_cast<float (*)[64]>(dst + BC::STAGE), lane);
@@ -249,6 +263,15 @@ kl_bwd_fused_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict_
     f32x16 acc[MAXIT];
     int r0;
   };
+  // read offsets of this wave's column blocks (wave, wave + 4, ...; those of
+  // the first distribution follow the second's)
+  DqOffsets dqo[MAXIT];
+#pragma unroll
+  for (int m = 0; m < MAXIT; ++m) {
+    const int it = wave + 4 * m;
+    if (C::WANT_B && it < C::NCB_B) dqo[m] = dq_offsets<C::CB>(lane, it);
+    else if constexpr (C::WANT_A) dqo[m] = dq_offsets<C::CA>(lane, it - C::NCB_B);
+  }
   auto dq_compute = [&](int t, DqWork& w) {
     w.r0 = t * C::BS;
     const int qlast = min(w.r0 + C::BS, NQ) - 1;
@@ -260,9 +283,9 @@ kl_bwd_fused_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict_
       const int it = wave + 4 * m;
       if (it < C::ITEMS) {
         if (C::WANT_B && it < C::NCB_B)
-          w.acc[m] = dq_block_mma<C::CB, C::BR / 16>(ds_b, kres_b, it, jend, lane);
+          w.acc[m] = dq_block_mma<C::CB, C::BR / 16>(ds_b, kres_b, dqo[m], jend);
         else if constexpr (C::WANT_A)
-          w.acc[m] = dq_block_mma<C::CA, C::BR / 16>(ds_a, kres_a, it - C::NCB_B, jend, lane);
+          w.acc[m] = dq_block_mma<C::CA, C::BR / 16>(ds_a, kres_a, dqo[m], jend);
       }
     }
   };
@@ -347,7 +370,7 @@ kl_bwd_fused_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict_
     if (prev >= 0) barrier_no_fence();
     if constexpr (C::WANT_A) store_ds(ds_a, kloc, half, dsa);
     if constexpr (C::WANT_B) store_ds(ds_b, kloc, half, dsb);
-    if (active) bwd_grad_tile<DA, DB, MODE>(cur, dsa, dsb, dka, dkb, ln);
+    if (active) bwd_grad_tile<DA, DB, MODE>(cur, dsa, dsb, dka, dkb, tro);
     if (has_next) {
       // vector memory operations complete in issue order: with the last 16
       // (atomics) allowed in flight, the next tile's loads are done
