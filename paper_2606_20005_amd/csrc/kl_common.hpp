@@ -221,6 +221,64 @@ struct TileDma {
 };
 
 // ---------------------------------------------------------------------------
+// Row-padded tile layout (forward key tiles). Each row of CPR chunks gets P
+// slots; its chunks sit in the order 0, 2, 4, ..., 1, 3, 5, ... from slot
+// rot(r) of the row. An MFMA operand lane of row r reads chunks 2 ks + half,
+// ks = 0, 1, ...: in this layout they are contiguous from
+// base(r, half) = r P + rot(r) + half CPR / 2, so one base register and
+// immediate offsets address all of them. P = 8 (mod 16) and rot(r) =
+// (r / 2) mod 8 put 16 consecutive rows at one position into 16 distinct
+// groups of four banks (the read is conflict-free); the remaining P - CPR
+// slots of a row are padding.
+// ---------------------------------------------------------------------------
+template <int CPR>
+struct PadRows {
+  static constexpr int P = CPR <= 16 ? 24 : 40;
+  static_assert(CPR % 8 == 0 && CPR <= 32, "rows of 8 to 32 chunks");
+  __host__ __device__ static constexpr int rot(int r) { return (r >> 1) & 7; }
+  __host__ __device__ static constexpr int base(int r, int half) { return r * P + rot(r) + half * (CPR / 2); }
+};
+
+// Direct-to-LDS staging of R rows of A (CA chunks) and B (CB chunks) into the
+// row-padded layout (R P_A + R P_B slots). Slot s of a tensor holds row
+// s / P, position p = s mod P - rot(row); positions outside 0 .. CPR - 1 are
+// padding and reload the row's first chunk.
+template <int R, int CA, int CB, int NT>
+struct PadTileDma {
+  static constexpr int PA = PadRows<CA>::P, PB = PadRows<CB>::P;
+  static constexpr int NCH_A = R * PA / NT, NCH = NCH_A + R * PB / NT;
+  static_assert((R * PA) % NT == 0 && (R * PB) % NT == 0, "staging split");
+  uint32_t voff[NCH];
+
+  template <int CPR, int P>
+  __device__ __forceinline__ static uint32_t chunk_of(int s) {
+    const int r = s / P, p = s - r * P - PadRows<CPR>::rot(r);
+    const int c = (p < 0 || p >= CPR) ? 0 : (p < CPR / 2 ? 2 * p : 2 * (p - CPR / 2) + 1);
+    return (uint32_t)(r * CPR + c) * 16u;
+  }
+  __device__ __forceinline__ explicit PadTileDma(int tid) {
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      const int p = tid + NT * i;
+      voff[i] = i < NCH_A ? chunk_of<CA, PA>(p) : chunk_of<CB, PB>(p - R * PA);
+    }
+  }
+  __device__ __forceinline__ void issue(rsrc_t ra, rsrc_t rb, int row0, u32x4* stage, int wave) const {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const uint32_t base_a = (uint32_t)row0 * CA * 16u, base_b = (uint32_t)row0 * CB * 16u;
+#pragma unroll
+    for (int i = 0; i < NCH_A; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(stage + NT * i + 64 * wave), 16,
+                                               voff[i] + base_a, 0, 0, 0);
+#pragma unroll
+    for (int i = NCH_A; i < NCH; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void*)(stage + NT * i + 64 * wave), 16,
+                                               voff[i] + base_b, 0, 0, 0);
+#endif
+  }
+};
+
+// ---------------------------------------------------------------------------
 // Workgroup -> tile mapping. The dispatcher hands workgroup w to XCD w % 8,
 // and each XCD has its own L2. Renumber so that XCD x receives a contiguous
 // range of logical tiles: the workgroups resident on one XCD then belong to

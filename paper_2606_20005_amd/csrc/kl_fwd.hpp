@@ -137,25 +137,38 @@ __device__ __forceinline__ void fwd_update_second(RowState& st, TileCarry& tc, c
 }
 
 // S^T of one key tile on the MFMA: A = key rows from LDS, B = the lane's
-// resident query rows; the two accumulation chains alternate.
-template <int DA, int DB>
+// resident query rows; the two accumulation chains alternate. PAD: the tile
+// is in the row-padded layout and base_a, base_b are the lane's operand
+// bases (chunk slots); otherwise it is swizzled and the addresses are
+// recomputed here.
+template <int DA, int DB, bool PAD>
 __device__ __forceinline__ void fwd_logits(const u32x4* stage, const bf16x8 (&qa)[DA / 16],
-                                           const bf16x8 (&qb)[DB / 16], f32x16& sa, f32x16& sb, int lane) {
+                                           const bf16x8 (&qb)[DB / 16], f32x16& sa, f32x16& sb, int lane,
+                                           int base_a, int base_b) {
   constexpr int KA = DA / 16, KB = DB / 16, KM = KA > KB ? KA : KB;
   constexpr int CA = DA / 8, CB = DB / 8;
-  const int half = lane >> 5;
-  // Recompute the swizzled operand addresses on every call rather than keep
-  // them live across the loop: the logits wave has vector cycles to spare,
-  // the update state has no registers to spare.
-  int r = lane & 31;
-  asm volatile("" : "+v"(r));
-  const u32x4* ta = stage;
-  const u32x4* tb = stage + kFwdBK * CA;
   f32x16 acc_a = zero16(), acc_b = zero16();
+  if constexpr (PAD) {
+    const u32x4* ta = stage + base_a;
+    const u32x4* tb = stage + kFwdBK * PadRows<CA>::P + base_b;
 #pragma unroll
-  for (int ks = 0; ks < KM; ++ks) {
-    if (ks < KA) acc_a = mfma32(lds_row8<CA>(ta, r, 2 * ks + half), qa[ks], acc_a);
-    if (ks < KB) acc_b = mfma32(lds_row8<CB>(tb, r, 2 * ks + half), qb[ks], acc_b);
+    for (int ks = 0; ks < KM; ++ks) {
+      if (ks < KA) acc_a = mfma32(__builtin_bit_cast(bf16x8, ta[ks]), qa[ks], acc_a);
+      if (ks < KB) acc_b = mfma32(__builtin_bit_cast(bf16x8, tb[ks]), qb[ks], acc_b);
+    }
+  } else {
+    const int half = lane >> 5;
+    // Recompute the swizzled operand addresses on every call rather than keep
+    // them live across the loop: the update state has no registers to spare.
+    int r = lane & 31;
+    asm volatile("" : "+v"(r));
+    const u32x4* ta = stage;
+    const u32x4* tb = stage + kFwdBK * CA;
+#pragma unroll
+    for (int ks = 0; ks < KM; ++ks) {
+      if (ks < KA) acc_a = mfma32(lds_row8<CA>(ta, r, 2 * ks + half), qa[ks], acc_a);
+      if (ks < KB) acc_b = mfma32(lds_row8<CB>(tb, r, 2 * ks + half), qb[ks], acc_b);
+    }
   }
   // Keep LOOKAHEAD operand reads in flight ahead of the MFMA that consumes
   // them: with one logits wave per SIMD nothing else hides the LDS latency.
@@ -257,7 +270,7 @@ __device__ __forceinline__ WaveTiles wave_tiles(int qw, int wlast, int NQ, int N
 // stage tile t - 1 occupied; after tile t + 1 has landed, (NSTAGE - 2) tiles
 // of loads are still in flight.
 // ----------------------------------------------------------------------------
-template <int DA_, int DB_, int NSTAGE_, int MINB_, int NW_ = 4>
+template <int DA_, int DB_, int NSTAGE_, int MINB_, int NW_ = 4, bool PAD_ = false>
 struct FwdTraits {
   static constexpr int DA = DA_, DB = DB_;
   static constexpr int NW = NW_;                            // waves per workgroup
@@ -265,10 +278,15 @@ struct FwdTraits {
   static constexpr int BQ = 32 * NW;                        // query rows per workgroup
   static constexpr int BK = kFwdBK;
   static constexpr int CA = DA / 8, CB = DB / 8;
-  static constexpr int STAGE = BK * (CA + CB);
+  // key tiles in the row-padded layout (one operand base register) or swizzled
+  static constexpr bool PAD = PAD_;
+  static constexpr int SA = PAD ? PadRows<CA>::P : CA, SB = PAD ? PadRows<CB>::P : CB;   // slots per row
+  static constexpr int STAGE = BK * (SA + SB);
   static constexpr int NSTAGE = NSTAGE_;
-  // threads that stream the key tiles: 512 when that splits both tensors' chunks evenly, else 256
-  static constexpr int DMA_NT = (NT >= 512 && (BK * CA) % 512 == 0 && (BK * CB) % 512 == 0) ? 512 : (NT < 256 ? NT : 256);
+  // threads that stream the key tiles: the most (of 512, 384, 256, 128, 64, up to the workgroup) that split both
+  // tensors' slots into whole loads
+  static constexpr bool splits(int n) { return n <= NT && (BK * SA) % n == 0 && (BK * SB) % n == 0; }
+  static constexpr int DMA_NT = splits(512) ? 512 : splits(384) ? 384 : splits(256) ? 256 : splits(128) ? 128 : 64;
   static constexpr int NCH = STAGE / DMA_NT;                // direct-to-LDS loads per streaming thread per tile
   static constexpr int MINB = MINB_;                        // workgroups per CU the registers are sized for
   static_assert(DA % 64 == 0 && DB % 64 == 0, "head dims must be multiples of 64");
@@ -306,8 +324,13 @@ __device__ __forceinline__ RowPartial fwd_pass(u32x4* smem, const uint16_t* __re
 
   const rsrc_t rka = make_rsrc(Ka + (size_t)bh * NK * DA, (uint32_t)NK * DA * 2u);
   const rsrc_t rkb = make_rsrc(Kb + (size_t)bh * NK * DB, (uint32_t)NK * DB * 2u);
-  const TileDma<BK, C::CA, C::CB, C::DMA_NT> dma(tid & (C::DMA_NT - 1));
+  using Dma = typename std::conditional<C::PAD, PadTileDma<BK, C::CA, C::CB, C::DMA_NT>,
+                                        TileDma<BK, C::CA, C::CB, C::DMA_NT>>::type;
   const bool streamer = wave < C::DMA_NT / 64;
+  const Dma dma(streamer ? tid : 0);
+  // operand bases of the row-padded layout (unused otherwise)
+  const int base_a = C::PAD ? PadRows<C::CA>::base(lane & 31, half) : 0;
+  const int base_b = C::PAD ? PadRows<C::CB>::base(lane & 31, half) : 0;
   RowState st{kNegInf, 0.f, kNegInf, 0.f, 0.f};
   TileCarry tc{};
   auto stage_of = [&](int t) { return smem + ((t - t_begin) % R) * C::STAGE; };
@@ -322,7 +345,7 @@ __device__ __forceinline__ RowPartial fwd_pass(u32x4* smem, const uint16_t* __re
     if (streamer) dma.issue(rka, rkb, (t + R - 1) * BK, stage_of(t + R - 1), wave);
     if (t <= wt.tlast) {
       f32x16 sa, sb;
-      fwd_logits<DA, DB>(stage_of(t), qa, qb, sa, sb, lane);
+      fwd_logits<DA, DB, C::PAD>(stage_of(t), qa, qb, sa, sb, lane, base_a, base_b);
       if (t >= wt.tmask) mask_tile(sa, sb, t * BK + 4 * half, NK, kcm);
       fwd_update_first(st, tc, sa, sb, ca, cb);
       fwd_update_second(st, tc, sa, sb, ca, cb);
@@ -404,7 +427,8 @@ kl_fwd_merge_kernel(const float* __restrict__ part, int W, size_t rows, float* _
 // tile), a two-stage ring and two workgroups per CU while the Q operands fit
 // 128 registers per lane; wider heads take four waves and one workgroup.
 template <int DA, int DB>
-using FwdCfg = typename std::conditional<(DA + DB <= 256), FwdTraits<DA, DB, 2, 2, 8>, FwdTraits<DA, DB, 2, 1, 4>>::type;
+using FwdCfg = typename std::conditional<(DA + DB <= 256), FwdTraits<DA, DB, 2, 2, 8, true>,
+                                         FwdTraits<DA, DB, 2, 1, 4, true>>::type;
 
 // Few query rows per head (decode-like shapes): NW waves per workgroup; four
 // one-wave or two four-wave workgroups per CU (one for wide heads).
