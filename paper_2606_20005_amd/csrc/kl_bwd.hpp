@@ -50,6 +50,15 @@ struct RowStats {
   float dl;          // (LSE_a - LSE_b) + L
 };
 
+// Fold |g| into the exponent offsets of a row: g P_t = 2^(c_t raw - (LSE_t log2 e - log2 |g|)).
+// A row with g = 0 gets +inf offsets (its P terms become 0).
+__device__ __forceinline__ RowStats fold_row_stats(RowStats s) {
+  const float l2g = __builtin_amdgcn_logf(fabsf(s.g));   // log2 |g|; -inf at 0
+  s.lsa2 -= l2g;
+  s.lsb2 -= l2g;
+  return s;
+}
+
 __device__ __forceinline__ RowStats load_row_stats(const float* kl, const float* lse_a, const float* lse_b,
                                                    const float* g, size_t ri, bool valid) {
   RowStats s{0.f, 0.f, 0.f, 0.f};
@@ -94,12 +103,15 @@ struct RowsDma {
   }
 };
 
-// Statistics of a streamed 32-row tile in LDS: [lsa2, lsb2, g, dl][row].
+// Statistics of a streamed 32-row tile in LDS: [lsa2, lsb2, g, dl][row], and
+// in *fold whether g has been folded into lsa2, lsb2 (every g of the tile
+// >= 0, the usual case; the stored g is then 1): the tile loop may then skip
+// one multiply per distribution and element. Rows at tid >= BS idle.
 template <int BS>
 __device__ __forceinline__ void stage_row_stats(const float (*raw)[64], int r0, int NQ, bool has_g,
-                                                f32x4 (&dst)[4][BS / 4], int tid) {
+                                                f32x4 (&dst)[4][BS / 4], int* fold, int tid) {
+  RowStats s{0.f, 0.f, 0.f, 0.f};
   if (tid < BS) {
-    RowStats s{0.f, 0.f, 0.f, 0.f};
     const float la = raw[0][tid];
     if (r0 + tid < NQ && la != kNegInf) {   // padding and rows with no allowed key contribute nothing
       const float lb = raw[1][tid];
@@ -108,16 +120,27 @@ __device__ __forceinline__ void stage_row_stats(const float (*raw)[64], int r0, 
       s.g = has_g ? raw[3][tid] : 1.f;
       s.dl = (la - lb) + raw[2][tid];
     }
+  }
+  const bool any_negative = __builtin_amdgcn_ballot_w64(tid < BS && s.g < 0.f) != 0;
+  if (tid < BS) {
+    if (!any_negative) {   // g = 1 keeps the unfolded path exact on a folded tile
+      s = fold_row_stats(s);
+      s.g = 1.f;
+    }
     float* p = reinterpret_cast<float*>(&dst[0][0]);
     p[0 * BS + tid] = s.lsa2;
     p[1 * BS + tid] = s.lsb2;
     p[2 * BS + tid] = s.g;
     p[3 * BS + tid] = s.dl;
+    if (tid == 0) *fold = any_negative ? 0 : 1;
   }
 }
 
-// Logit gradients of one element (raw dot products ra, rb).
-template <bool WANT_A, bool WANT_B>
+// Logit gradients of one element (raw dot products ra, rb). FOLD: the row's
+// |g| is already folded into the exponent offsets (lsa2, lsb2 lowered by
+// log2 |g|), so the exponentials are g P directly and the sign of g is
+// applied elsewhere; otherwise g multiplies here.
+template <bool WANT_A, bool WANT_B, bool FOLD = false>
 __device__ __forceinline__ void dlogits(float ra, float rb, bool ok, float ca, float cb, float sa, float sb,
                                         const RowStats& s, float& dsa, float& dsb) {
   const float xa = ok ? __builtin_fmaf(ra, ca, -s.lsa2) : kNegInf;
@@ -125,13 +148,14 @@ __device__ __forceinline__ void dlogits(float ra, float rb, bool ok, float ca, f
   if constexpr (WANT_B) {
     const float xb = ok ? __builtin_fmaf(rb, cb, -s.lsb2) : kNegInf;
     const float pb = exp2_fast(xb);
-    dsb = s.g * (pb - pa);
+    dsb = FOLD ? pb - pa : s.g * (pb - pa);
   }
   if constexpr (WANT_A) {
     const float u = __builtin_fmaf(ra, sa, -__builtin_fmaf(rb, sb, s.dl));
-    dsa = (s.g * pa) * u;
+    dsa = FOLD ? pa * u : (s.g * pa) * u;
   }
 }
+
 
 // ----------------------------------------------------------------------------
 // One streamed tile of one wave, shared by all backward kernels. The wave owns
@@ -143,7 +167,8 @@ __device__ __forceinline__ void dlogits(float ra, float rb, bool ok, float ca, f
 // allowed pair.
 // ----------------------------------------------------------------------------
 // ra_op(ks), rb_op(ks) return the resident operands of k-step ks (16 columns).
-template <int DA, int DB, int MODE, bool MASK, typename OpA, typename OpB, typename StatsFn, typename OkFn>
+template <int DA, int DB, int MODE, bool MASK, bool FOLD, typename OpA, typename OpB, typename StatsFn,
+          typename OkFn>
 __device__ __forceinline__ void bwd_dlogits_tile(const u32x4* stage, OpA ra_op, OpB rb_op, float ca, float cb,
                                                  float sa, float sb, int lane, StatsFn stats, OkFn ok,
                                                  float (&dsa)[16], float (&dsb)[16]) {
@@ -160,7 +185,7 @@ __device__ __forceinline__ void bwd_dlogits_tile(const u32x4* stage, OpA ra_op, 
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     const RowStats rs = stats(i);
-    dlogits<C::WANT_A, C::WANT_B>(s_a[i], s_b[i], MASK ? ok(i) : true, ca, cb, sa, sb, rs, dsa[i], dsb[i]);
+    dlogits<C::WANT_A, C::WANT_B, FOLD>(s_a[i], s_b[i], MASK ? ok(i) : true, ca, cb, sa, sb, rs, dsa[i], dsb[i]);
   }
 }
 
@@ -237,7 +262,7 @@ __device__ __forceinline__ void bwd_grad_tile(const u32x4* stage, const float (&
   }
 }
 
-template <int DA, int DB, int MODE, bool MASK, typename StatsFn, typename OkFn>
+template <int DA, int DB, int MODE, bool MASK, bool FOLD, typename StatsFn, typename OkFn>
 __device__ __forceinline__ void bwd_tile(const u32x4* stage, const bf16x8 (&ra_op)[DA / 16],
                                          const bf16x8 (&rb_op)[DB / 16],
                                          f32x16 (&ga)[(MODE & 2) ? DA / 32 : 1],
@@ -245,8 +270,9 @@ __device__ __forceinline__ void bwd_tile(const u32x4* stage, const bf16x8 (&ra_o
                                          float ca, float cb, float sa, float sb, int lane,
                                          StatsFn stats, OkFn ok, const TrOffsets<DA, DB, MODE>& to) {
   float dsa[16], dsb[16];
-  bwd_dlogits_tile<DA, DB, MODE, MASK>(stage, [&](int ks) { return ra_op[ks]; }, [&](int ks) { return rb_op[ks]; },
-                                       ca, cb, sa, sb, lane, stats, ok, dsa, dsb);
+  bwd_dlogits_tile<DA, DB, MODE, MASK, FOLD>(stage, [&](int ks) { return ra_op[ks]; },
+                                             [&](int ks) { return rb_op[ks]; }, ca, cb, sa, sb, lane, stats, ok,
+                                             dsa, dsb);
   bwd_grad_tile<DA, DB, MODE>(stage, dsa, dsb, ga, gb, to);
 }
 
@@ -262,20 +288,27 @@ __device__ __forceinline__ void load_resident(bf16x8 (&op)[D / 16], const uint16
 }
 
 // Write one gradient tile: lane l, register i holds row base + 8 (i / 4) + 4 half + i % 4,
-// column 32 nb + l % 32; the factor s of S = s Q K^T is applied here.
-template <int D>
+// column 32 nb + l % 32; the factor s of S = s Q K^T is applied here, times
+// row_scale(i) when given.
+template <int D, typename RowScale>
 __device__ __forceinline__ void write_grad(float* out, const f32x16 (&acc)[D / 32], size_t bh_rows, int base,
-                                           int n, float s, int lane) {
+                                           int n, float s, int lane, RowScale row_scale) {
   const int half = lane >> 5;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     const int row = base + 8 * (i >> 2) + 4 * half + (i & 3);
     if (row < n) {
+      const float f = s * row_scale(i);
       float* o = out + (bh_rows + row) * D + (lane & 31);
 #pragma unroll
-      for (int nb = 0; nb < D / 32; ++nb) o[32 * nb] = acc[nb][i] * s;
+      for (int nb = 0; nb < D / 32; ++nb) o[32 * nb] = acc[nb][i] * f;
     }
   }
+}
+template <int D>
+__device__ __forceinline__ void write_grad(float* out, const f32x16 (&acc)[D / 32], size_t bh_rows, int base,
+                                           int n, float s, int lane) {
+  write_grad<D>(out, acc, bh_rows, base, n, s, lane, [](int) { return 1.f; });
 }
 
 // ----------------------------------------------------------------------------
@@ -316,7 +349,11 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
     ntiles = kmax < 0 ? 0 : min(ntiles, kmax / C::BS + 1);
   }
 
-  const RowStats rs = load_row_stats(kl, lse_a, lse_b, g, (size_t)bh * NQ + myq, myq < NQ);
+  // |g| of the lane's row goes into its exponent offsets, its sign into the
+  // written row
+  const RowStats rs0 = load_row_stats(kl, lse_a, lse_b, g, (size_t)bh * NQ + myq, myq < NQ);
+  const float gsign = rs0.g < 0.f ? -1.f : 1.f;
+  const RowStats rs = fold_row_stats(rs0);
   bf16x8 qa[DA / 16], qb[DB / 16];
   load_resident<DA>(qa, Qa, (size_t)bh * NQ, myq, NQ, half);
   load_resident<DB>(qb, Qb, (size_t)bh * NQ, myq, NQ, half);
@@ -351,9 +388,9 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
       return k < NK && k <= kmax_ok;
     };
     if (opaque(need_mask))
-      bwd_tile<DA, DB, MODE, true>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, lane, stats, ok, tro);
+      bwd_tile<DA, DB, MODE, true, true>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, lane, stats, ok, tro);
     else
-      bwd_tile<DA, DB, MODE, false>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, lane, stats, ok, tro);
+      bwd_tile<DA, DB, MODE, false, true>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, lane, stats, ok, tro);
   };
 
   if (ntiles > 0) dma.issue(rka, rkb, 0, st0, wave);
@@ -370,8 +407,15 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
     if (kt + 1 < ntiles) step(st1, st0, kt + 1);
   }
 
-  if constexpr (C::WANT_B) write_grad<DB>(dQb, dqb, (size_t)bh * NQ, qw, NQ, sb, lane);
-  if constexpr (C::WANT_A) write_grad<DA>(dQa, dqa, (size_t)bh * NQ, qw, NQ, sa, lane);
+  // register i holds the row of lane 8 (i / 4) + 4 half + i % 4
+  float rsign[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i)
+    rsign[i] = __int_as_float(
+        __builtin_amdgcn_ds_bpermute(4 * (8 * (i >> 2) + 4 * half + (i & 3)), __float_as_int(gsign)));
+  auto row_sign = [&](int i) { return rsign[i]; };
+  if constexpr (C::WANT_B) write_grad<DB>(dQb, dqb, (size_t)bh * NQ, qw, NQ, sb, lane, row_sign);
+  if constexpr (C::WANT_A) write_grad<DA>(dQa, dqa, (size_t)bh * NQ, qw, NQ, sa, lane, row_sign);
 }
 
 // ----------------------------------------------------------------------------
@@ -391,6 +435,7 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   __shared__ u32x4 st1[C::STAGE];
   __shared__ f32x4 sstat[2][4][C::BS / 4];    // their row statistics: [stage][lsa2, lsb2, g, dl][rows / 4]
   __shared__ float sraw[4][64];               // saved row values of the next tile, as loaded
+  __shared__ int sfold[2];                    // per stage: g folded into the statistics
 
   // the wave index is uniform: in a scalar register, so are the values derived from it
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), half = lane >> 5;
@@ -435,7 +480,8 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   };
 
   const TrOffsets<DA, DB, MODE> tro(lane);
-  auto tile = [&](const u32x4* stage, const f32x4 (&st)[4][C::BS / 4], int t) {
+  auto tile = [&](const u32x4* stage, int buf, int t) {
+    const f32x4 (&st)[4][C::BS / 4] = sstat[buf];
     const int r0 = t * C::BS;
     bool active = kw < NK;
     bool need_mask = r0 + C::BS > NQ;
@@ -454,24 +500,26 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
       const int q = r0 + 8 * (i >> 2) + 4 * half + (i & 3);
       return q < NQ && (!CAUSAL || myk <= q + off);
     };
-    if (opaque(need_mask))
-      bwd_tile<DA, DB, MODE, true>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, lane, stats, ok, tro);
+    // the general path also takes the tiles whose g could not be folded
+    // (a third variant would cost registers everywhere)
+    if (opaque(need_mask || !sfold[buf]))
+      bwd_tile<DA, DB, MODE, true, false>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, lane, stats, ok, tro);
     else
-      bwd_tile<DA, DB, MODE, false>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, lane, stats, ok, tro);
+      bwd_tile<DA, DB, MODE, false, true>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, lane, stats, ok, tro);
   };
 
   if (t_begin < ntq) {
     stage_in(t_begin, st0);
     wait_vmem();
-    stage_row_stats<C::BS>(sraw, t_begin * C::BS, NQ, rdma.has_g, sstat[0], tid);
+    stage_row_stats<C::BS>(sraw, t_begin * C::BS, NQ, rdma.has_g, sstat[0], &sfold[0], tid);
   }
   __syncthreads();
   auto step = [&](const u32x4* cur, u32x4* nxt, int t, int buf) {
     const bool has_next = t + 1 < ntq;
     if (has_next) stage_in(t + 1, nxt);
-    tile(cur, sstat[buf], t);
+    tile(cur, buf, t);
     wait_vmem();
-    if (has_next) stage_row_stats<C::BS>(sraw, (t + 1) * C::BS, NQ, rdma.has_g, sstat[buf ^ 1], tid);
+    if (has_next) stage_row_stats<C::BS>(sraw, (t + 1) * C::BS, NQ, rdma.has_g, sstat[buf ^ 1], &sfold[buf ^ 1], tid);
     __syncthreads();
   };
   for (int t = t_begin; t < ntq; t += 2) {

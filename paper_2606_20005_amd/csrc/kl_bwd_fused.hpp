@@ -57,7 +57,7 @@ struct FusedCfg {
   static constexpr int DS_CH = BR * BS * 2 / 16;           // one dS tile (bf16)
   static constexpr int NDS = (WANT_A ? 1 : 0) + (WANT_B ? 1 : 0);
   static constexpr int CHUNKS = RING + KRES_A + KRES_B + NDS * DS_CH;
-  static constexpr int LDS_BYTES = 16 * CHUNKS + 2 * 4 * BS * 4 + 2 * 4 * 64 * 4;
+  static constexpr int LDS_BYTES = 16 * CHUNKS + 2 * 4 * BS * 4 + 2 * 4 * 64 * 4 + 16;
   static constexpr int LDS_LIMIT = 160 * 1024;
   static constexpr bool FITS = LDS_BYTES <= LDS_LIMIT;
   static constexpr int MINB = (Base::MINB == 2 && 2 * LDS_BYTES <= LDS_LIMIT) ? 2 : 1;
@@ -174,6 +174,7 @@ kl_bwd_fused_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict_
   __shared__ u32x4 ds_a[C::WANT_A ? C::DS_CH : 1];                  // dS tiles
   __shared__ u32x4 ds_b[C::WANT_B ? C::DS_CH : 1];
   __shared__ f32x4 sstat[2][4][C::BS / 4];                          // row statistics of the stages
+  __shared__ int sfold[2];                                          // per stage: g folded into them
   auto raw_of = [](const u32x4* stage) { return reinterpret_cast<const float (*)[64]>(stage + BC::STAGE); };
 
   // the wave index is uniform: in a scalar register, so are the values derived from it
@@ -358,10 +359,11 @@ kl_bwd_fused_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict_
     float dsa[16], dsb[16];
     asm volatile("" : "+v"(kres_row));
     if (active) {
-      if (opaque(need_mask))
-        bwd_dlogits_tile<DA, DB, MODE, true>(cur, op_a, op_b, ca, cb, sa, sb, ln, stats, ok, dsa, dsb);
+      // the general path also takes the tiles whose g could not be folded
+      if (opaque(need_mask || !sfold[buf]))
+        bwd_dlogits_tile<DA, DB, MODE, true, false>(cur, op_a, op_b, ca, cb, sa, sb, ln, stats, ok, dsa, dsb);
       else
-        bwd_dlogits_tile<DA, DB, MODE, false>(cur, op_a, op_b, ca, cb, sa, sb, ln, stats, ok, dsa, dsb);
+        bwd_dlogits_tile<DA, DB, MODE, false, true>(cur, op_a, op_b, ca, cb, sa, sb, ln, stats, ok, dsa, dsb);
     } else {
 #pragma unroll
       for (int e = 0; e < 16; ++e) { dsa[e] = 0.f; dsb[e] = 0.f; }
@@ -376,7 +378,8 @@ kl_bwd_fused_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict_
       // (atomics) allowed in flight, the next tile's loads are done
       if (n_atomic >= 16) wait_vmem_le<16>();
       else wait_vmem();
-      stage_row_stats<C::BS>(raw_of(nxt), tile_at(i + 1) * C::BS, NQ, rdma.has_g, sstat[buf ^ 1], tid);
+      stage_row_stats<C::BS>(raw_of(nxt), tile_at(i + 1) * C::BS, NQ, rdma.has_g, sstat[buf ^ 1], &sfold[buf ^ 1],
+                             tid);
     }
     wait_lds();
     barrier_no_fence();
@@ -386,7 +389,7 @@ kl_bwd_fused_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict_
   if (nt > 0) {
     stage_in(tile_at(0), st0);
     wait_vmem();
-    stage_row_stats<C::BS>(raw_of(st0), tile_at(0) * C::BS, NQ, rdma.has_g, sstat[0], tid);
+    stage_row_stats<C::BS>(raw_of(st0), tile_at(0) * C::BS, NQ, rdma.has_g, sstat[0], &sfold[0], tid);
   }
   wait_vmem();   // key block copies
   __syncthreads();

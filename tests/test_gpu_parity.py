@@ -13,14 +13,14 @@ pytestmark = pytest.mark.gpu
 ALL = ("dq1", "dk1", "dq2", "dk2")
 
 
-def run_case(sk, d, causal, direction, want=ALL, use_g=True):
+def run_case(sk, d, causal, direction, want=ALL, use_g=True, strategy="separate"):
     import torch
     w = d["w"]
     q1, k1, q2, k2 = upload(d)
     kl, l1, l2 = sk.fwd(q1, k1, q2, k2, w.s1, w.s2, causal, direction)
     g_np = d["g"] if use_g else None
     g = to_gpu_f32(g_np) if use_g else None
-    grads = sk.bwd(q1, k1, q2, k2, kl, l1, l2, g, w.s1, w.s2, causal, direction, want=want)
+    grads = sk.bwd(q1, k1, q2, k2, kl, l1, l2, g, w.s1, w.s2, causal, direction, want=want, strategy=strategy)
     torch.cuda.synchronize()
     ref = oracle.backward(d["Q1"], d["K1"], d["Q2"], d["K2"], w.s1, w.s2, causal, direction, g_np)
     check_rows("kl", kl.cpu().numpy(), ref[0])
@@ -86,6 +86,35 @@ def test_gradient_subsets(gpu_lib, want, direction):
 
 def test_upstream_gradient_none_is_ones(gpu_lib):
     run_case(gpu_lib, inputs.make("tiny", n_q=130, n_k=190), True, 0, use_g=False)
+
+
+def _signed_g(shape, pattern):
+    rng = np.random.default_rng(11)
+    g = rng.uniform(0.5, 1.5, size=shape).astype(np.float32)
+    if pattern == "mixed":            # random signs: almost every 32-row tile holds a negative g
+        g *= rng.choice(np.float32([-1, 1]), size=shape)
+    elif pattern == "some_tiles":     # one negative row in every other 32-row tile, zeros elsewhere
+        g[..., 40::64] *= -1
+        g[..., 3::50] = 0.0
+        g[..., 7::64] = -0.0
+    elif pattern == "magnitudes":     # |g| over many binades, zeros, signs
+        g *= np.float32(2.0) ** rng.integers(-60, 40, size=shape).astype(np.float32)
+        g[..., 5::9] *= -1
+        g[..., ::13] = 0.0
+    return g
+
+
+@pytest.mark.parametrize("strategy", ["separate", "fused"])
+@pytest.mark.parametrize("pattern", ["mixed", "some_tiles", "magnitudes"])
+def test_upstream_gradient_signs(gpu_lib, pattern, strategy):
+    """The kernels fold |g| of a row into its exponent offsets when they can
+    (dQ: every row, the sign applied when written; dK: tiles whose g are all
+    >= 0) and multiply by g otherwise: negative, zero and widely scaled g
+    give the oracle's gradients on either side of that choice."""
+    d = inputs.make("tiny", B=1, H=2, n_q=200, n_k=700)
+    d["g"] = _signed_g(d["g"].shape, pattern)
+    for causal in (False, True):
+        run_case(gpu_lib, d, causal, 0, strategy=strategy)
 
 
 @pytest.mark.parametrize("name,over,causal", [
