@@ -157,6 +157,21 @@ __device__ __forceinline__ void dlogits(float ra, float rb, bool ok, float ca, f
 }
 
 
+// Wave priority around the matrix phases of a tile. Two waves share a SIMD:
+// while one issues its MFMA chain at raised priority, the other's vector
+// work fills the issue slots the chain leaves, which measured 3-4% faster
+// for one gradient pair. With both pairs (twice the gradient MFMAs per
+// tile) the raised priority starves the other wave's vector phase and
+// measured 5% slower, so mode 3 keeps the default.
+template <int MODE>
+__device__ __forceinline__ void mfma_phase_begin() {
+  if constexpr (MODE != 3) __builtin_amdgcn_s_setprio(1);
+}
+template <int MODE>
+__device__ __forceinline__ void mfma_phase_end() {
+  if constexpr (MODE != 3) __builtin_amdgcn_s_setprio(0);
+}
+
 // ----------------------------------------------------------------------------
 // One streamed tile of one wave, shared by all backward kernels. The wave owns
 // 32 resident rows (queries for dQ, keys for dK) held as MFMA B operands
@@ -178,10 +193,12 @@ __device__ __forceinline__ void bwd_dlogits_tile(const u32x4* stage, OpA ra_op, 
   const u32x4* tb = stage + C::BS * C::CA;
   const int r = lane & 31;
   f32x16 s_a = zero16(), s_b = zero16();
+  mfma_phase_begin<MODE>();
 #pragma unroll
   for (int ks = 0; ks < DA / 16; ++ks) s_a = mfma32(lds_row8<C::CA>(ta, r, 2 * ks + half), ra_op(ks), s_a);
 #pragma unroll
   for (int ks = 0; ks < DB / 16; ++ks) s_b = mfma32(lds_row8<C::CB>(tb, r, 2 * ks + half), rb_op(ks), s_b);
+  mfma_phase_end<MODE>();
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     const RowStats rs = stats(i);
@@ -239,6 +256,7 @@ __device__ __forceinline__ void bwd_grad_tile(const u32x4* stage, const float (&
                                               f32x16 (&gb)[(MODE & 1) ? DB / 32 : 1],
                                               const TrOffsets<DA, DB, MODE>& to) {
   using C = BwdCfg<DA, DB, MODE>;
+  mfma_phase_begin<MODE>();
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
     if constexpr (C::WANT_B) {
@@ -260,6 +278,7 @@ __device__ __forceinline__ void bwd_grad_tile(const u32x4* stage, const float (&
       }
     }
   }
+  mfma_phase_end<MODE>();
 }
 
 template <int DA, int DB, int MODE, bool MASK, bool FOLD, typename StatsFn, typename OkFn>
