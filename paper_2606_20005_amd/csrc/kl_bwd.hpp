@@ -453,7 +453,10 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   __shared__ u32x4 st0[C::STAGE];             // two stages of query tiles (two arrays: see the dQ kernel)
   __shared__ u32x4 st1[C::STAGE];
   __shared__ f32x4 sstat[2][4][C::BS / 4];    // their row statistics: [stage][lsa2, lsb2, g, dl][rows / 4]
-  __shared__ float sraw[4][64];               // saved row values of the next tile, as loaded
+  // saved row values as loaded, one tile ahead of the tiles (two arrays for
+  // the same reason as the stages; tile t_begin + 2j uses the first)
+  __shared__ float sraw0[4][64];
+  __shared__ float sraw1[4][64];
   __shared__ int sfold[2];                    // per stage: g folded into the statistics
 
   // the wave index is uniform: in a scalar register, so are the values derived from it
@@ -493,10 +496,6 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   const TileDma<C::BS, C::CA, C::CB> dma(tid);
 
   const RowsDma rdma(kl, lse_a, lse_b, g, (size_t)bh * NQ, NQ);
-  auto stage_in = [&](int t, u32x4* dst) {
-    dma.issue(rqa, rqb, t * C::BS, dst, wave);
-    if (wave == 0) rdma.issue(t * C::BS, sraw, lane);
-  };
 
   const TrOffsets<DA, DB, MODE> tro(lane);
   auto tile = [&](const u32x4* stage, int buf, int t) {
@@ -527,23 +526,34 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
       bwd_tile<DA, DB, MODE, false, true>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, lane, stats, ok, tro);
   };
 
+  // The row values of tile t + 1 are turned into statistics by wave 0 early
+  // in step t, while the tile is computed: they were loaded with the
+  // previous tile, so no wait sits between the end-of-step wait and barrier.
+  auto stats_in = [&](int t, float (*raw)[64], int buf) {
+    if (wave == 0) stage_row_stats<C::BS>(raw, t * C::BS, NQ, rdma.has_g, sstat[buf], &sfold[buf], tid);
+  };
   if (t_begin < ntq) {
-    stage_in(t_begin, st0);
+    dma.issue(rqa, rqb, t_begin * C::BS, st0, wave);
+    if (wave == 0) {
+      rdma.issue(t_begin * C::BS, sraw0, lane);
+      if (t_begin + 1 < ntq) rdma.issue((t_begin + 1) * C::BS, sraw1, lane);
+    }
     wait_vmem();
-    stage_row_stats<C::BS>(sraw, t_begin * C::BS, NQ, rdma.has_g, sstat[0], &sfold[0], tid);
+    stats_in(t_begin, sraw0, 0);
   }
   __syncthreads();
-  auto step = [&](const u32x4* cur, u32x4* nxt, int t, int buf) {
-    const bool has_next = t + 1 < ntq;
-    if (has_next) stage_in(t + 1, nxt);
+  // rnext holds the row values of tile t + 1; rfree receives those of t + 2
+  auto step = [&](const u32x4* cur, u32x4* nxt, float (*rnext)[64], float (*rfree)[64], int t, int buf) {
+    if (t + 1 < ntq) dma.issue(rqa, rqb, (t + 1) * C::BS, nxt, wave);
+    if (wave == 0 && t + 2 < ntq) rdma.issue((t + 2) * C::BS, rfree, lane);
+    if (t + 1 < ntq) stats_in(t + 1, rnext, buf ^ 1);
     tile(cur, buf, t);
     wait_vmem();
-    if (has_next) stage_row_stats<C::BS>(sraw, (t + 1) * C::BS, NQ, rdma.has_g, sstat[buf ^ 1], &sfold[buf ^ 1], tid);
     __syncthreads();
   };
   for (int t = t_begin; t < ntq; t += 2) {
-    step(st0, st1, t, 0);
-    if (t + 1 < ntq) step(st1, st0, t + 1, 1);
+    step(st0, st1, sraw1, sraw0, t, 0);
+    if (t + 1 < ntq) step(st1, st0, sraw0, sraw1, t + 1, 1);
   }
 
   if constexpr (C::WANT_B) write_grad<DB>(dKb, dkb, (size_t)bh * NK, kw, NK, sb, lane);
