@@ -126,3 +126,49 @@ def test_fullsize_long_causal(gpu_lib):
 
 def test_fullsize_indexer_causal(gpu_lib):
     _run_full(gpu_lib, "indexer", True, full_stats_ok=False)
+
+
+@pytest.mark.parametrize("n_q", [1, 16, 64])
+def test_fullsize_decode_split_and_fused(gpu_lib, n_q):
+    """The decode-like shapes that the split-K and backward-strategy figures
+    time (16 heads, N_K = 65536, d1 = d2 = 128, non-causal), through the
+    adaptive paths: the split-K forward and the fused backward the rule picks.
+    Every query row of three heads and sampled keys of one head against the
+    oracle; the fused gradients against the separate kernels' on all heads."""
+    import torch
+    t0 = time.time()
+    d = inputs.make("mid", B=16, H=1, n_q=n_q, n_k=65536)
+    w = d["w"]
+    _log(f"[fullsize] decode n_q={n_q}: B={w.B} H={w.H} NK={w.n_k} d={w.d1}")
+    q1, k1, q2, k2 = upload(d)
+    g = to_gpu_f32(d["g"])
+    assert gpu_lib.split_count(w.B, w.H, n_q, w.n_k, w.d1, w.d2) > 1
+    assert gpu_lib.bwd_choose(w.B, w.H, n_q, w.n_k, w.d1, w.d2) == "fused"
+    kl, l1, l2 = gpu_lib.fwd_split(q1, k1, q2, k2, w.s1, w.s2, False, 0, splits="auto")
+    want = ("dq2", "dk2")
+    fused = gpu_lib.bwd(q1, k1, q2, k2, kl, l1, l2, g, w.s1, w.s2, False, 0, want=want, strategy="auto")
+    sep = gpu_lib.bwd(q1, k1, q2, k2, kl, l1, l2, g, w.s1, w.s2, False, 0, want=want, strategy="separate")
+    torch.cuda.synchronize()
+    _log(f"[fullsize] decode n_q={n_q}: GPU passes {time.time() - t0:.1f} s")
+    assert float(kl.min()) >= -KL_ATOL
+    for name, f, s in zip(("dq2", "dk2"), fused[2:], sep[2:]):
+        rel = float((f.double() - s.double()).norm() / s.double().norm())
+        assert rel <= 1e-5, (name, rel)
+
+    rng = np.random.default_rng(w.seed + n_q)
+    args = (d["Q1"], d["K1"], d["Q2"], d["K2"], w.s1, w.s2, False, 0)
+    rows = np.arange(n_q)
+    for b_ in sorted({0, w.B - 1, int(rng.integers(w.B))}):
+        rk, r1, r2 = oracle.forward_rows(*args, b_, 0, rows)
+        check_rows("kl", kl[b_, 0].cpu().numpy(), rk)
+        check_rows("lse1", l1[b_, 0].cpu().numpy(), r1)
+        check_rows("lse2", l2[b_, 0].cpu().numpy(), r2)
+        _, rq2 = oracle.dq_rows(*args, b_, 0, rows, d["g"][b_, 0, rows])
+        check_grad("dq2", fused[2][b_, 0].cpu().numpy(), rq2)
+    b_ = w.B - 1
+    keys = np.unique(np.concatenate([[0, 1, 127, 128, w.n_k // 2, w.n_k - 1], rng.choice(w.n_k, 40, replace=False)]))
+    _, rk2 = oracle.dk_rows(*args, b_, 0, keys, d["g"][b_, 0])
+    kidx = torch.as_tensor(keys, device=kl.device)
+    e = check_grad("dk2", fused[3][b_, 0, kidx].cpu().numpy(), rk2)
+    _log(f"[fullsize] decode n_q={n_q}: rows and {keys.size} keys ok, dK2 rel L2 {e:.2e}; "
+         f"total {time.time() - t0:.1f} s")
