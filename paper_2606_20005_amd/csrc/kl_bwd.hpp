@@ -51,9 +51,13 @@ struct RowStats {
 };
 
 // Fold |g| into the exponent offsets of a row: g P_t = 2^(c_t raw - (LSE_t log2 e - log2 |g|)).
-// A row with g = 0 gets +inf offsets (its P terms become 0).
+// A row with g = 0 gets +inf offsets (its P terms become 0). Subnormal |g|
+// is scaled into the normal range first (the hardware log2 flushes
+// subnormal inputs).
 __device__ __forceinline__ RowStats fold_row_stats(RowStats s) {
-  const float l2g = __builtin_amdgcn_logf(fabsf(s.g));   // log2 |g|; -inf at 0
+  const float a = fabsf(s.g);
+  const bool tiny = a < 0x1p-126f;
+  const float l2g = __builtin_amdgcn_logf(tiny ? a * 0x1p64f : a) - (tiny ? 64.f : 0.f);   // -inf at 0
   s.lsa2 -= l2g;
   s.lsb2 -= l2g;
   return s;
