@@ -315,7 +315,7 @@ def main():
              "dk": "kl_bwd_dk_kernel<128,128,mode1>"}
     achieved = kern[dom]["tflops"]
     res = {
-        "metric": "fused attn-KL fwd+bwd TFLOP/s (algorithmic) at N=16K; per-pass ms, TFLOP/s, % bf16 MFMA peak; extra HBM",
+        "metric": "fused attn-KL fwd/bwd TFLOP/s + ms at N=16K/64K; % bf16 MFMA peak; extra HBM",
         "value": round(value, 2),
         "unit": "TFLOP/s",
         "n_gpus": 1,
