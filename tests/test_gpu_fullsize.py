@@ -172,3 +172,55 @@ def test_fullsize_decode_split_and_fused(gpu_lib, n_q):
     e = check_grad("dk2", fused[3][b_, 0, kidx].cpu().numpy(), rk2)
     _log(f"[fullsize] decode n_q={n_q}: rows and {keys.size} keys ok, dK2 rel L2 {e:.2e}; "
          f"total {time.time() - t0:.1f} s")
+
+
+def test_maximum_key_extent(gpu_lib):
+    """The largest key count the boundary accepts at d1 = d2 = 256: one head's
+    fp32 dK slab is just under 4 GiB (2^32 - 1024 bytes), the limit of the
+    32-bit slab offsets. Few query rows, so the adaptive paths run (split-K
+    forward, fused backward); both agree with the single-pass forward and the
+    separate backward kernels, and every row and sampled keys (first, around
+    2^21, the ragged last tile) match the oracle."""
+    import torch
+    t0 = time.time()
+    n_k = 4194303
+    assert gpu_lib.lib.streamkl_fwd(None, None, None, None, 1, 1, 8, n_k + 1, 256, 256, 0.0625, 0.0625, 0, 0,
+                                    None, None, None, None) == gpu_lib.ERR_UNSUPPORTED
+    d = inputs.make("tiny", B=1, H=1, n_q=8, n_k=n_k, d1=256, d2=256, s1=0.0625, s2=0.0625)
+    w = d["w"]
+    _log(f"[fullsize] max extent: NK={n_k} d=256, inputs {time.time() - t0:.1f} s")
+    q1, k1, q2, k2 = upload(d)
+    g = to_gpu_f32(d["g"])
+    want = ("dq2", "dk2")
+    for causal in (False, True):
+        kl, l1, l2 = gpu_lib.fwd_split(q1, k1, q2, k2, w.s1, w.s2, causal, 0, splits="auto")
+        one = gpu_lib.fwd(q1, k1, q2, k2, w.s1, w.s2, causal, 0)
+        grads = gpu_lib.bwd(q1, k1, q2, k2, kl, l1, l2, g, w.s1, w.s2, causal, 0, want=want, strategy="auto")
+        torch.cuda.synchronize()
+        for a, b in zip((kl, l1, l2), one):
+            assert torch.allclose(a, b, rtol=2e-5, atol=2e-5)
+        sep = gpu_lib.bwd(q1, k1, q2, k2, kl, l1, l2, g, w.s1, w.s2, causal, 0, want=want, strategy="separate")
+        torch.cuda.synchronize()
+        # the same fp32 sums over 4M keys in two orders (atomics over key
+        # blocks against one accumulator per row)
+        for name, f, s in zip(want, grads[2:], sep[2:]):
+            rel = float((f.double() - s.double()).norm() / s.double().norm())
+            assert rel <= 1e-4, (name, rel)
+        sep_dq2 = sep[2][0, 0].cpu().numpy()
+        del sep
+        _log(f"[fullsize] max extent causal={causal}: GPU passes done, {time.time() - t0:.1f} s")
+        args = (d["Q1"], d["K1"], d["Q2"], d["K2"], w.s1, w.s2, causal, 0)
+        rows = np.arange(w.n_q)
+        rk, r1, r2 = oracle.forward_rows(*args, 0, 0, rows)
+        check_rows("kl", kl[0, 0].cpu().numpy(), rk)
+        check_rows("lse1", l1[0, 0].cpu().numpy(), r1)
+        check_rows("lse2", l2[0, 0].cpu().numpy(), r2)
+        check_rows("kl (single pass)", one[0][0, 0].cpu().numpy(), rk)
+        _, rq2 = oracle.dq_rows(*args, 0, 0, rows, d["g"][0, 0, rows])
+        check_grad("dq2", grads[2][0, 0].cpu().numpy(), rq2)
+        check_grad("dq2 (separate)", sep_dq2, rq2)
+        keys = np.array([0, 1, 2 ** 21 - 1, 2 ** 21, n_k - 33, n_k - 32, n_k - 2, n_k - 1])   # n_k - 1 = 2^22 - 1
+        _, rk2 = oracle.dk_rows(*args, 0, 0, keys, d["g"][0, 0])
+        e = check_grad("dk2", grads[3][0, 0, torch.as_tensor(keys, device=kl.device)].cpu().numpy(), rk2)
+        _log(f"[fullsize] max extent causal={causal}: oracle ok, dK2 rel L2 {e:.2e}, {time.time() - t0:.1f} s")
+        del grads
