@@ -224,3 +224,45 @@ def test_maximum_key_extent(gpu_lib):
         e = check_grad("dk2", grads[3][0, 0, torch.as_tensor(keys, device=kl.device)].cpu().numpy(), rk2)
         _log(f"[fullsize] max extent causal={causal}: oracle ok, dK2 rel L2 {e:.2e}, {time.time() - t0:.1f} s")
         del grads
+
+
+def test_maximum_query_extent(gpu_lib):
+    """The largest query count the boundary accepts at d1 = d2 = 256 (one
+    head's fp32 dQ slab just under 4 GiB), with 64 keys: the single-pass
+    forward and the separate backward kernels (the rule's choice here) on
+    sampled rows against the oracle, dK2 of every key, and the identity
+    <dQ2, Q2> = <dK2, K2> over the whole head. Causal (bottom-right) leaves all
+    but the last 64 rows without a visible key: KL 0, LSE -inf, zero dQ."""
+    import torch
+    t0 = time.time()
+    n_q, n_k = 4194303, 64
+    d = inputs.make("tiny", B=1, H=1, n_q=n_q, n_k=n_k, d1=256, d2=256, s1=0.0625, s2=0.0625)
+    w = d["w"]
+    _log(f"[fullsize] max query extent: NQ={n_q} NK={n_k} d=256, inputs {time.time() - t0:.1f} s")
+    q1, k1, q2, k2 = upload(d)
+    g = to_gpu_f32(d["g"])
+    assert gpu_lib.bwd_choose(1, 1, n_q, n_k, 256, 256) == "separate"
+    rng = np.random.default_rng(17)
+    for causal in (False, True):
+        kl, l1, l2 = gpu_lib.fwd(q1, k1, q2, k2, w.s1, w.s2, causal, 0)
+        _, _, dq2, dk2 = gpu_lib.bwd(q1, k1, q2, k2, kl, l1, l2, g, w.s1, w.s2, causal, 0, want=("dq2", "dk2"))
+        torch.cuda.synchronize()
+        _log(f"[fullsize] max query extent causal={causal}: GPU passes done, {time.time() - t0:.1f} s")
+        a = float((dq2.double() * q2.double()).sum())
+        b = float((dk2.double() * k2.double()).sum())
+        scale = float((dq2.double() * q2.double()).sum(dim=3).abs().sum())
+        assert abs(a - b) <= PROPERTY_REL * scale, (a, b, scale)
+        args = (d["Q1"], d["K1"], d["Q2"], d["K2"], w.s1, w.s2, causal, 0)
+        rows = np.unique(np.concatenate([[0, 1, 2 ** 21, n_q - 65, n_q - 64, n_q - 2, n_q - 1],
+                                         rng.choice(n_q, 24, replace=False)]))
+        ridx = torch.as_tensor(rows, device=kl.device)
+        rk, r1, r2 = oracle.forward_rows(*args, 0, 0, rows)
+        check_rows("kl", kl[0, 0, ridx].cpu().numpy(), rk)
+        check_rows("lse1", l1[0, 0, ridx].cpu().numpy(), r1)
+        check_rows("lse2", l2[0, 0, ridx].cpu().numpy(), r2)
+        _, rq2 = oracle.dq_rows(*args, 0, 0, rows, d["g"][0, 0, rows])
+        check_grad("dq2", dq2[0, 0, ridx].cpu().numpy(), rq2)
+        _, rk2 = oracle.dk_rows(*args, 0, 0, np.arange(n_k), d["g"][0, 0], row_block=1 << 20)
+        e = check_grad("dk2", dk2[0, 0].cpu().numpy(), rk2)
+        _log(f"[fullsize] max query extent causal={causal}: oracle ok, dK2 rel L2 {e:.2e}, {time.time() - t0:.1f} s")
+        del kl, l1, l2, dq2, dk2
