@@ -24,8 +24,8 @@
  *   and must be 16-byte aligned. Row statistics and gradients are fp32,
  *   contiguous, 4-byte aligned: kl, lse1, lse2, dkl are [B, H, N_Q];
  *   dQ1 [B,H,N_Q,d1], dQ2 [B,H,N_Q,d2], dK1 [B,H,N_K,d1], dK2 [B,H,N_K,d2].
- * - s1, s2 are the logit scales (the paper omits sqrt(d) "for brevity"; the
- *   usual choice is 1/sqrt(d_t)). They must be finite and > 0.
+ * - s1, s2 are the logit scales (the paper leaves the sqrt(d) factor out of
+ *   its formulas; the usual choice is 1/sqrt(d_t)). They must be finite and > 0.
  * - causal = 1 masks with bottom-right alignment: query row i sits at
  *   absolute position N_K - N_Q + i and attends keys j <= that position
  *   (j <= i when N_Q = N_K). Rows left with no key (only when N_Q > N_K)

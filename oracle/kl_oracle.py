@@ -27,8 +27,8 @@ the logits; nothing is fused, blocked across keys or reordered.
 Readings where the paper is silent (the same list is kept with the design
 notes of the repository):
 
-* scale: S_t = s_t Q_t K_t^T with independent s1, s2 (the paper omits
-  sqrt(d) "for brevity"); s_t is an fp32 argument of the operation, so it is
+* scale: S_t = s_t Q_t K_t^T with independent s1, s2 (the paper leaves
+  the sqrt(d) factor out of its formulas); s_t is an fp32 argument of the operation, so it is
   rounded to fp32 before use.
 * causal masking: bottom-right alignment. Query row i sits at absolute
   position N_K - N_Q + i and may attend keys j <= that position (inclusive);
