@@ -266,3 +266,38 @@ def test_maximum_query_extent(gpu_lib):
         e = check_grad("dk2", dk2[0, 0].cpu().numpy(), rk2)
         _log(f"[fullsize] max query extent causal={causal}: oracle ok, dK2 rel L2 {e:.2e}, {time.time() - t0:.1f} s")
         del kl, l1, l2, dq2, dk2
+
+
+def test_fullsize_distill_reverse_all_gradients(gpu_lib):
+    """The distillation workload (teacher d1 = 128, student d2 = 64, causal)
+    in the reverse direction KL(P2 || P1) with all four gradients (the
+    both-settings kernels), on sampled rows and keys of two heads."""
+    import torch
+    t0 = time.time()
+    d = inputs.make("distill")
+    w = d["w"]
+    q1, k1, q2, k2 = upload(d)
+    g = to_gpu_f32(d["g"])
+    kl, l1, l2 = gpu_lib.fwd(q1, k1, q2, k2, w.s1, w.s2, True, 1)
+    grads = gpu_lib.bwd(q1, k1, q2, k2, kl, l1, l2, g, w.s1, w.s2, True, 1, want=("dq1", "dk1", "dq2", "dk2"))
+    torch.cuda.synchronize()
+    _log(f"[fullsize] distill reverse: GPU passes {time.time() - t0:.1f} s")
+    assert float(kl.min()) >= -KL_ATOL
+    rng = np.random.default_rng(w.seed + 1)
+    args = (d["Q1"], d["K1"], d["Q2"], d["K2"], w.s1, w.s2, True, 1)
+    for b_, h_ in ((0, 0), (w.B - 1, w.H - 1)):
+        rows = _sample_rows(w.n_q, rng, k=24)
+        ridx = torch.as_tensor(rows, device=kl.device)
+        rk, r1, r2 = oracle.forward_rows(*args, b_, h_, rows)
+        check_rows("kl", kl[b_, h_, ridx].cpu().numpy(), rk)
+        check_rows("lse1", l1[b_, h_, ridx].cpu().numpy(), r1)
+        check_rows("lse2", l2[b_, h_, ridx].cpu().numpy(), r2)
+        rq1, rq2 = oracle.dq_rows(*args, b_, h_, rows, d["g"][b_, h_, rows])
+        check_grad("dq1", grads[0][b_, h_, ridx].cpu().numpy(), rq1)
+        check_grad("dq2", grads[2][b_, h_, ridx].cpu().numpy(), rq2)
+        keys = _sample_keys(w, True, rng, True, k=16)
+        kidx = torch.as_tensor(keys, device=kl.device)
+        rk1, rk2 = oracle.dk_rows(*args, b_, h_, keys, d["g"][b_, h_], row_block=512)
+        check_grad("dk1", grads[1][b_, h_, kidx].cpu().numpy(), rk1)
+        check_grad("dk2", grads[3][b_, h_, kidx].cpu().numpy(), rk2)
+        _log(f"[fullsize] distill reverse: head ({b_},{h_}) ok, {time.time() - t0:.1f} s")
