@@ -12,10 +12,13 @@ d1=d2=128, s=1/sqrt(128), non-causal, student Q2 = bf16(Q1 + 0.3 eps), K2 = K1.
 Prints ONE JSON line. The 64K causal long-context figures (d1=128, d2=64,
 outlier channels) ride along in "long_context" unless --no-64k, and the
 split-K forward on decode-like shapes (16 heads of 1-64 query rows over 64K
-keys) in "split_k" unless --no-split, and the separate against the fused
-backward on the same shapes in "fused_bwd" unless --no-fused.
+keys) in "split_k" unless --no-split, the separate against the fused
+backward on the same shapes in "fused_bwd" unless --no-fused, and the
+per-pass figures of the other causal workloads (distill, mid, indexer) in
+"workloads" unless --no-workloads.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-64k] [--no-cpu-baseline] [--no-split] [--no-fused]
+                    [--no-workloads]
 """
 from __future__ import annotations
 
@@ -289,6 +292,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-split", action="store_true", help="skip the split-K decode-shape figures")
     ap.add_argument("--no-fused", action="store_true", help="skip the fused-backward decode-shape figures")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the per-pass figures of the other workloads (distill, mid causal, indexer)")
     ap.add_argument("--causal", action="store_true", help="run the 16K workload with causal masking")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run one 1 GiB device copy (reference kernel for HBM counters)")
@@ -355,6 +360,21 @@ def main():
             "dq_ms": kern_l["dq"]["ms"], "dq_tflops": kern_l["dq"]["tflops"],
             "dk_ms": kern_l["dk"]["ms"], "dk_tflops": kern_l["dk"]["tflops"], "extra_hbm": extra_l,
             "naive_p1_p2_bytes": 2 * 2 * P_l, "kl_mean": kl_l}
+    if not a.no_workloads:
+        rows = []
+        for name, wc in (("distill", True), ("mid", True), ("indexer", True)):
+            wo = inputs.WORKLOADS[name]
+            ms_o, wall_o, _, kl_o = run_workload(sk, wo, wc, 3, 1)
+            kern_o, P_o, f_o = summarize(wo, wc, ms_o)
+            rows.append({"workload": f"{name}: B={wo.B} H={wo.H} N_Q={wo.n_q} N_K={wo.n_k} d1={wo.d1} d2={wo.d2} "
+                                     + ("causal" if wc else "non-causal"),
+                         "pairs": P_o, "ms_per_step": round(wall_o, 4),
+                         **{f"{k}_ms": kern_o[k]["ms"] for k in ("fwd", "dq", "dk")},
+                         **{f"{k}_frac_bf16_peak": kern_o[k]["frac_bf16_peak"] for k in ("fwd", "dq", "dk")},
+                         "step_tflops_algorithmic": round(
+                             (f_o["fwd"] + f_o["bwd_algorithmic"]) * P_o / (wall_o * 1e-3) / 1e12, 2),
+                         "kl_mean": kl_o})
+        res["workloads"] = rows
     if not a.no_split:
         res["split_k"] = split_k_figures(sk)
     if not a.no_fused:
