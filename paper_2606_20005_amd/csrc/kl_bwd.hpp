@@ -17,6 +17,8 @@
 // contraction, K (for dQ) or Q (for dK), is read from the same LDS tile with
 // gfx950 transpose reads (ds_read_b64_tr_b16). The factor s_t of
 // S_t = s_t Q_t K_t^T is applied once when the gradient tile is written.
+// Where it can, a kernel folds |g| of a row into the row's exponent offsets
+// (fold_row_stats), so that the exponentials are g P directly.
 //
 // MODE bit 0: produce the gradient of "b" (Setting 1); bit 1: of "a" (Setting 2).
 #pragma once
@@ -81,9 +83,10 @@ __device__ __forceinline__ RowStats load_row_stats(const float* kl, const float*
 
 // Saved values (LSE_a, LSE_b, L and, when given, g) of 64 consecutive query
 // rows of one head, brought into LDS raw[4][64] by direct-to-LDS dword loads
-// that travel with the tile loads (rows past N_Q read as zeros). One wave
-// issues them; after its wait for the tile, stage_row_stats turns the 32 rows
-// of the tile into the form the inner loop uses.
+// issued by one wave together with tile loads (rows past N_Q read as zeros;
+// the dK kernel loads them one tile ahead). Once they have landed,
+// stage_row_stats turns the 32 rows of a tile into the form the inner loop
+// uses.
 struct RowsDma {
   rsrc_t r_la, r_lb, r_kl, r_g;
   bool has_g;

@@ -8,7 +8,9 @@
 // the tile, so every row reduction is in-lane: the two half-waves (l / 32 =
 // 0, 1) hold disjoint key subsets of the same rows and each keeps its own five
 // running scalars, merged once at the end by the split-K rule of Sec. 3.3.
-// Nothing crosses lanes inside the key loop.
+// Nothing crosses lanes inside the key loop. Every kFoldTiles tiles a lane
+// also folds its scalars into a per-lane total in LDS by the same rule, which
+// bounds the number of additions any fp32 running sum takes.
 //
 // Arithmetic is in the base-2 domain (Sec. 5 uses exp2): t = raw * s * log2(e),
 // p = 2^(t - m), and acc = sum p_a (t_a - t_b) (eq:acc-invariant in base 2, so
@@ -29,8 +31,8 @@
 // passes (Q1,K1) as a for KL(P1||P2) and swaps the roles for KL(P2||P1).
 //
 // One kernel serves every head-dim pair; its configuration (waves per
-// workgroup, ring depth, workgroups per CU) is chosen per pair at the end of
-// this file. Every wave forms its own logits and runs its own online update:
+// workgroup, workgroups per CU, key-tile layout) is chosen per pair at the
+// end of this file. Every wave forms its own logits and runs its own online update:
 // on gfx950 this update is bound by vector and transcendental issue (two
 // exp2 per pair), and variants that hand the matrix work to separate waves
 // in barrier-separated phases measured slower (an MFMA stream slows the
