@@ -38,15 +38,20 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 
 
 def kernel_source_hash():
-    """SHA-256 over the HIP sources and the C header: counters are only valid for the code they measured."""
+    """SHA-256 over the code of the HIP sources and the C header: counters are only valid for the code they
+    measured. Comments and layout are left out, so editing a comment keeps the measurement."""
     import glob
     import hashlib
+    import re
     h = hashlib.sha256()
     files = sorted(glob.glob(os.path.join(ROOT, "paper_2606_20005_amd", "csrc", "*"))) + \
         [os.path.join(ROOT, "include", "streamkl.h")]
     for f in files:
         with open(f, "rb") as fh:
-            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+            text = fh.read()
+        text = re.sub(rb"/\*.*?\*/", b" ", text, flags=re.S)
+        text = re.sub(rb"//[^\n]*", b"", text)
+        h.update(os.path.basename(f).encode() + b"\0" + b" ".join(text.split()))
     return h.hexdigest()
 
 
