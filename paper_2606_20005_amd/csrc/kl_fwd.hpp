@@ -450,21 +450,32 @@ kl_fwd_partial_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restric
   }
 }
 
-// Split-K reduce (Sec. 3.3): one thread per row merges its W partial states
-// and writes KL, LSE_a, LSE_b.
-__global__ void __launch_bounds__(256)
+// Split-K reduce (Sec. 3.3): one wave per row. Lane w merges partials w,
+// w + 64, ... (independent loads, all in flight together), then the wave
+// merges its 64 lane states by a butterfly of shuffles, and lane 0 writes
+// KL, LSE_a, LSE_b. One thread per row walking its W partials in sequence
+// spent a load latency per partial: 14-20 us at W = 32.
+constexpr int kMergeRowsPerBlock = 4;
+__global__ void __launch_bounds__(64 * kMergeRowsPerBlock)
 kl_fwd_merge_kernel(const float* __restrict__ part, int W, size_t rows, float* __restrict__ kl,
                     float* __restrict__ lse_a, float* __restrict__ lse_b) {
-  const size_t ri = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (ri >= rows) return;
+  const int lane = threadIdx.x & 63;
+  const size_t ri = (size_t)blockIdx.x * kMergeRowsPerBlock + (threadIdx.x >> 6);
+  if (ri >= rows) return;   // whole waves leave together
   const size_t plane = (size_t)W * rows;
   RowPartial acc{kNegInf, 0.f, kNegInf, 0.f, 0.f};
-  for (int w = 0; w < W; ++w) {
+  for (int w = lane; w < W; w += 64) {
     const size_t i = (size_t)w * rows + ri;
     acc = merge_partials(acc, RowPartial{part[i], part[i + plane], part[i + 2 * plane], part[i + 3 * plane],
                                          part[i + 4 * plane]});
   }
-  write_row(acc, ri, kl, lse_a, lse_b);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const RowPartial other{__shfl_xor(acc.ma, off), __shfl_xor(acc.la, off), __shfl_xor(acc.mb, off),
+                           __shfl_xor(acc.lb, off), __shfl_xor(acc.acc, off)};
+    acc = merge_partials(acc, other);
+  }
+  if (lane == 0) write_row(acc, ri, kl, lse_a, lse_b);
 }
 
 // Configuration per head-dim pair: eight waves (256 rows share each key

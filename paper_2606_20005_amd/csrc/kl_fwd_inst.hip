@@ -23,7 +23,8 @@ static hipError_t run_cfg(const FwdArgs& a, int W, float* part) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t rows = (size_t)a.BH * a.NQ;
-  hipLaunchKernelGGL(kl_fwd_merge_kernel, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, a.stream,
+  hipLaunchKernelGGL(kl_fwd_merge_kernel, dim3((unsigned)((rows + kMergeRowsPerBlock - 1) / kMergeRowsPerBlock)),
+                     dim3(64 * kMergeRowsPerBlock), 0, a.stream,
                      part, W, rows, a.kl, a.lse_a, a.lse_b);
   return hipGetLastError();
 }
@@ -35,6 +36,8 @@ static hipError_t run_fwd(const FwdArgs& a, int W, float* part) {
     if (a.NQ <= 128) return run_cfg<DA, DB, CAUSAL, FwdSmallCfg<DA, DB, 4>>(a, W, part);
   return run_cfg<DA, DB, CAUSAL, FwdCfg<DA, DB>>(a, W, part);
 }
+
+int fwd_merge_rows_per_workgroup() { return kMergeRowsPerBlock; }
 
 int fwd_rows_per_workgroup(int da, int db, int n_q) {
   if (n_q <= 32) return 32;

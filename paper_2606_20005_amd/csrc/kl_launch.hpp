@@ -33,6 +33,8 @@ struct BwdArgs {
 hipError_t launch_fwd(int da, int db, bool causal, const FwdArgs& a, int W, float* part);
 // Query rows per workgroup of the forward for these head dims and rows per head.
 int fwd_rows_per_workgroup(int da, int db, int n_q);
+// Rows per workgroup of the split-K merge.
+int fwd_merge_rows_per_workgroup();
 hipError_t launch_bwd_dq(int da, int db, bool causal, int mode, const BwdArgs& a);
 hipError_t launch_bwd_dk(int da, int db, bool causal, int mode, const BwdArgs& a);
 hipError_t launch_bwd_dq_m1(int da, int db, bool causal, const BwdArgs& a);

@@ -79,7 +79,9 @@ int fwd_common(const void* Q1, const void* K1, const void* Q2, const void* K2, i
     const long long grid = (long long)B * H *
                            ((N_Q + streamkl::fwd_rows_per_workgroup(d1, d2, N_Q) - 1) /
                             streamkl::fwd_rows_per_workgroup(d1, d2, N_Q)) * splits;
-    if (grid > kMaxGrid || rows * splits > (1LL << 40)) return STREAMKL_ERR_UNSUPPORTED;
+    const long long merge_grid =
+        (rows + streamkl::fwd_merge_rows_per_workgroup() - 1) / streamkl::fwd_merge_rows_per_workgroup();
+    if (grid > kMaxGrid || merge_grid > kMaxGrid || rows * splits > (1LL << 40)) return STREAMKL_ERR_UNSUPPORTED;
     if (!empty && (!workspace || !aligned(workspace, 4) ||
                    workspace_bytes < streamkl_fwd_split_workspace_bytes(B, H, N_Q, splits)))
       return STREAMKL_ERR_INVALID_ARG;
