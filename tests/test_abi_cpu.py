@@ -201,3 +201,13 @@ def test_split_count_follows_the_adaptive_rule(sk):
     # invalid or unsupported
     assert sk.split_count(-1, 1, 1, 1, 128, 128) == 0
     assert sk.split_count(1, 1, 1, 1, 96, 128) == 0
+
+
+def test_split_merge_grid_limit(sk):
+    """2^34 rows split in two: every per-head extent and the partial grid are
+    within limits, but one merge workgroup per four rows would exceed the
+    launch grid; the call is refused before anything is launched."""
+    big = dict(B=1024, H=1024, NQ=16384, NK=64, splits=2, ws_bytes=1 << 62)
+    assert split_call(sk, **big) == 2
+    # 2^31 rows pass the grid checks and stop at the next one (no output pointer): nothing is launched
+    assert split_call(sk, **dict(big, B=128, kl=None)) == 1
