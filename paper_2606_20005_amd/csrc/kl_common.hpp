@@ -76,17 +76,10 @@ __device__ __forceinline__ bf16x8 lds_row8(const u32x4* tile, int r, int c) {
   return __builtin_bit_cast(bf16x8, tile[chunk_slot<CPR>(r, c)]);
 }
 
-// Transpose read: the calling lane addresses 4 bf16 at (row r, column e),
-// e a multiple of 4; see the layout note at the top of this file.
-template <int CPR>
-__device__ __forceinline__ bf16x4 lds_tr4(const u32x4* tile, int r, int e) {
-  const int byte = chunk_slot<CPR>(r, e >> 3) * 16 + ((e >> 2) & 1) * 8;
-  const lds_char* base = (const lds_char*)(tile);
-  i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + byte));
-  return __builtin_bit_cast(bf16x4, v);
-}
-
-// Transpose read at a byte offset of an LDS buffer with a layout of its own.
+// Transpose read at a byte offset of an LDS buffer. In a swizzled tile the
+// lane's 4 bf16 at (row r, column e), e a multiple of 4, sit at byte
+// chunk_slot(r, e / 8) * 16 + ((e / 4) % 2) * 8; see the layout note at the
+// top of this file.
 __device__ __forceinline__ bf16x4 lds_tr4_at(const void* buf, int byte) {
   const lds_char* base = (const lds_char*)(buf);
   i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + byte));
