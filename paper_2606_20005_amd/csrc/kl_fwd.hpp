@@ -485,6 +485,11 @@ template <int DA, int DB>
 using FwdCfg = typename std::conditional<(DA + DB <= 256), FwdTraits<DA, DB, 2, 2, 8, true>,
                                          FwdTraits<DA, DB, 2, 1, 4, true>>::type;
 
+// Causal heads with few 256-row blocks (the launcher's rule): four waves in
+// the default key-tile layout, two workgroups per CU.
+template <int DA, int DB>
+using FwdCausalSmallCfg = FwdTraits<DA, DB, 2, 2, 4, true>;
+
 // Few query rows per head (decode-like shapes): NW waves per workgroup; four
 // one-wave or two four-wave workgroups per CU (one for wide heads).
 template <int DA, int DB, int NW>

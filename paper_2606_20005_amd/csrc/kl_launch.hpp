@@ -31,8 +31,9 @@ struct BwdArgs {
 // W <= 1: one pass over all keys. W > 1: split-K (Sec. 3.3) with W key chunks;
 // part holds 5 * W * BH * NQ floats of partial row statistics.
 hipError_t launch_fwd(int da, int db, bool causal, const FwdArgs& a, int W, float* part);
-// Query rows per workgroup of the forward for these head dims and rows per head.
-int fwd_rows_per_workgroup(int da, int db, int n_q);
+// Query rows per workgroup of the forward for these head dims, rows per head,
+// number of heads and mask.
+int fwd_rows_per_workgroup(int da, int db, int n_q, long long bh, bool causal);
 // Rows per workgroup of the split-K merge.
 int fwd_merge_rows_per_workgroup();
 hipError_t launch_bwd_dq(int da, int db, bool causal, int mode, const BwdArgs& a);

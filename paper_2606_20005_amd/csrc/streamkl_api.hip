@@ -76,9 +76,8 @@ int fwd_common(const void* Q1, const void* K1, const void* Q2, const void* K2, i
   if (splits < 1) return STREAMKL_ERR_INVALID_ARG;
   if (splits > 1) {
     const long long rows = (long long)B * H * N_Q;
-    const long long grid = (long long)B * H *
-                           ((N_Q + streamkl::fwd_rows_per_workgroup(d1, d2, N_Q) - 1) /
-                            streamkl::fwd_rows_per_workgroup(d1, d2, N_Q)) * splits;
+    const int bq = streamkl::fwd_rows_per_workgroup(d1, d2, N_Q, (long long)B * H, causal == 1);
+    const long long grid = (long long)B * H * ((N_Q + bq - 1) / bq) * splits;
     const long long merge_grid =
         (rows + streamkl::fwd_merge_rows_per_workgroup() - 1) / streamkl::fwd_merge_rows_per_workgroup();
     if (grid > kMaxGrid || merge_grid > kMaxGrid || rows * splits > (1LL << 40)) return STREAMKL_ERR_UNSUPPORTED;
@@ -134,7 +133,7 @@ extern "C" int streamkl_fwd_split_count(int B, int H, int N_Q, int N_K, int d1, 
   if (B < 0 || H < 0 || N_Q < 0 || N_K < 0) return 0;
   if (!supported_dim(d1) || !supported_dim(d2)) return 0;
   constexpr long long kTarget = 512;   // two workgroups per CU on 256 CUs
-  const int bq = streamkl::fwd_rows_per_workgroup(d1, d2, N_Q);
+  const int bq = streamkl::fwd_rows_per_workgroup(d1, d2, N_Q, (long long)B * H, false);
   const long long base = (long long)B * H * ((N_Q + bq - 1) / bq);
   if (base == 0 || base >= kTarget) return 1;
   const long long tiles = (N_K + 31LL) / 32;
