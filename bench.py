@@ -195,6 +195,50 @@ def split_k_figures(sk, reps=10):
     return {"workload": f"B={B} H={H} N_K={NK} d1=d2={D} non-causal, N_Q in (1, 16, 32, 64)", "rows": out}
 
 
+def clock_figures(sk, reps=10):
+    """The mid forward (32 heads, 16384 x 16384, d = 128, non-causal) and a
+    library bf16 GEMM (torch.matmul, 8192^3) on seeded N(0,1) operands and on
+    constant operands of the same shapes: identical instruction streams, so a
+    difference in time is a difference in clock. The shader clock itself is
+    read under rocprofv3 --pmc GRBM_GUI_ACTIVE (cycles per dispatch, summed
+    over the eight XCDs, divided by the dispatch's duration)."""
+    import torch
+    w = {"B": 1, "H": 32, "n": 16384, "d": 128}
+    shape = (w["B"], w["H"], w["n"], w["d"])
+    s = w["d"] ** -0.5
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(2606200050 + 8)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    out = {"workload": "forward: B=1 H=32 N_Q=N_K=16384 d1=d2=128 non-causal; GEMM: bf16 8192 x 8192 x 8192 "
+                       "(torch.matmul, reference only)"}
+    fwd_flop = 2 * 2 * w["d"] * w["B"] * w["H"] * w["n"] * w["n"]
+    gemm_n = 8192
+    for label, make in (("randn", lambda sh: torch.randn(sh, generator=gen, device="cuda").to(torch.bfloat16)),
+                        ("ones", lambda sh: torch.ones(sh, device="cuda", dtype=torch.bfloat16))):
+        q1, k1, q2, k2 = (make(shape) for _ in range(4))
+        ms = timed(lambda: sk.fwd(q1, k1, q2, k2, s, s, False, 0))
+        out[f"fwd_ms_{label}"] = round(ms, 4)
+        out[f"fwd_tflops_{label}"] = round(fwd_flop / (ms * 1e-3) / 1e12, 2)
+        del q1, k1, q2, k2
+        a, b = make((gemm_n, gemm_n)), make((gemm_n, gemm_n))
+        ms = timed(lambda: torch.matmul(a, b))
+        out[f"gemm_tflops_{label}"] = round(2 * gemm_n ** 3 / (ms * 1e-3) / 1e12, 2)
+        del a, b
+    torch.cuda.empty_cache()
+    return out
+
+
 def fused_bwd_figures(sk, reps=10):
     """Backward strategies of Sec. 4.2 on the same decode-like shapes as the
     split-K figures (16 heads, N_K = 65536, d1 = d2 = 128, non-causal, student
@@ -300,6 +344,8 @@ def main():
     ap.add_argument("--no-workloads", action="store_true",
                     help="skip the per-pass figures of the other workloads (distill, mid causal, indexer)")
     ap.add_argument("--causal", action="store_true", help="run the 16K workload with causal masking")
+    ap.add_argument("--clock-probe", action="store_true",
+                    help="also time the mid forward and a library GEMM on random and on constant operands")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run one 1 GiB device copy (reference kernel for HBM counters)")
     a = ap.parse_args()
@@ -384,6 +430,8 @@ def main():
         res["split_k"] = split_k_figures(sk)
     if not a.no_fused:
         res["fused_bwd"] = fused_bwd_figures(sk)
+    if a.clock_probe:
+        res["clock_probe"] = clock_figures(sk)
     if a.copy_calibration:
         x = torch.empty(1 << 28, dtype=torch.float32, device="cuda")   # 1 GiB
         y = torch.empty_like(x)
