@@ -344,8 +344,8 @@ def main():
     ap.add_argument("--no-workloads", action="store_true",
                     help="skip the per-pass figures of the other workloads (distill, mid causal, indexer)")
     ap.add_argument("--causal", action="store_true", help="run the 16K workload with causal masking")
-    ap.add_argument("--clock-probe", action="store_true",
-                    help="also time the mid forward and a library GEMM on random and on constant operands")
+    ap.add_argument("--no-clock-probe", action="store_true",
+                    help="skip timing the mid forward and a library GEMM on random and on constant operands")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run one 1 GiB device copy (reference kernel for HBM counters)")
     a = ap.parse_args()
@@ -430,7 +430,7 @@ def main():
         res["split_k"] = split_k_figures(sk)
     if not a.no_fused:
         res["fused_bwd"] = fused_bwd_figures(sk)
-    if a.clock_probe:
+    if not a.no_clock_probe:
         res["clock_probe"] = clock_figures(sk)
     if a.copy_calibration:
         x = torch.empty(1 << 28, dtype=torch.float32, device="cuda")   # 1 GiB
