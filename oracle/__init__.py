@@ -12,10 +12,11 @@ Modules
 -------
 kl_oracle     the plain definition (Sec. 2.1, eq:kl-def / eq:kl-case1 /
               eq:kl-case2): explicit P1 and P2 row block by row block in fp64.
-online_model  Algorithm 1 (Sec. 3.2) executed tile by tile in fp64, plus the
-              split-K merge of Sec. 3.3. It is not the oracle; it pins the
-              paper's online derivation (eq:kl-final, eq:acc-invariant) to the
-              plain definition so that a GPU/oracle mismatch can be attributed.
+online_model  the online forward (Sec. 3.2) evaluated from per-tile partial
+              states folded with the split-K merge of Sec. 3.3, in fp64. It
+              is not the oracle; it pins the paper's online derivation
+              (eq:kl-final, eq:acc-invariant) to the plain definition so that
+              a GPU/oracle mismatch can be attributed.
 """
 from .kl_oracle import (  # noqa: F401
     forward,

@@ -40,6 +40,8 @@ struct BwdCfg {
   // tiles + about 80 for operands in flight, addresses and row statistics;
   // two waves per SIMD leave 256.
   static constexpr int REGS = (DA + DB) / 4 + 32 + (WANT_A ? DA / 2 : 0) + (WANT_B ? DB / 2 : 0) + 80;
+  // workgroups per CU; with four-wave workgroups also the waves per SIMD that
+  // __launch_bounds__ takes as its second argument
   static constexpr int MINB = REGS <= 248 ? 2 : 1;
   static_assert(DA % 64 == 0 && DB % 64 == 0, "head dims must be multiples of 64");
   static_assert(MODE >= 1 && MODE <= 3, "at least one gradient");

@@ -303,6 +303,10 @@ struct FwdTraits {
   static constexpr int DMA_NT = splits(512) ? 512 : splits(384) ? 384 : splits(256) ? 256 : splits(128) ? 128 : 64;
   static constexpr int NCH = STAGE / DMA_NT;                // direct-to-LDS loads per streaming thread per tile
   static constexpr int MINB = MINB_;                        // workgroups per CU the registers are sized for
+  // The second argument of __launch_bounds__ is waves per SIMD (execution
+  // unit), not workgroups per CU: MINB workgroups of NW waves spread over the
+  // four SIMDs of a CU.
+  static constexpr int WAVES_PER_SIMD = (MINB * NW + 3) / 4;
   static_assert(DA % 64 == 0 && DB % 64 == 0, "head dims must be multiples of 64");
   static_assert(NSTAGE >= 2, "tile shape");
 };
@@ -398,7 +402,7 @@ __device__ __forceinline__ RowPartial fwd_pass(u32x4* st0, u32x4* st1, float* to
 
 // Whole key range per workgroup: grid B*H * ceil(N_Q / BQ).
 template <class C, bool CAUSAL>
-__global__ void __launch_bounds__(C::NT, C::MINB)
+__global__ void __launch_bounds__(C::NT, C::WAVES_PER_SIMD)
 kl_fwd_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
               const uint16_t* __restrict__ Qb, const uint16_t* __restrict__ Kb,
               int NQ, int NK, float ca, float cb,
@@ -422,7 +426,7 @@ kl_fwd_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
 // writes the five row statistics to part[k][w][B*H*N_Q], k = (m_a, l_a, m_b,
 // l_b, acc), maxima in the base-2 domain.
 template <class C, bool CAUSAL>
-__global__ void __launch_bounds__(C::NT, C::MINB)
+__global__ void __launch_bounds__(C::NT, C::WAVES_PER_SIMD)
 kl_fwd_partial_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
                       const uint16_t* __restrict__ Qb, const uint16_t* __restrict__ Kb,
                       int NQ, int NK, float ca, float cb, int W, int chunk, float* __restrict__ part) {
@@ -479,10 +483,16 @@ kl_fwd_merge_kernel(const float* __restrict__ part, int W, size_t rows, float* _
 }
 
 // Configuration per head-dim pair: eight waves (256 rows share each key
-// tile), a two-stage ring and two workgroups per CU while the Q operands fit
-// 128 registers per lane; wider heads take four waves and one workgroup.
+// tile) and a two-stage ring. Two workgroups per CU (four waves per SIMD)
+// need the whole kernel in 128 registers per lane: the pairs up to d1 + d2 =
+// 192 and (128, 128) compile to at most 128 without spilling, (64, 192) and
+// (192, 64) need 136 and keep one workgroup per CU. Wider heads take four
+// waves and one workgroup. The launch bounds hold the compiler to these
+// occupancies; tests/test_build_resources.py checks them on the compiled code.
 template <int DA, int DB>
-using FwdCfg = typename std::conditional<(DA + DB <= 256), FwdTraits<DA, DB, 2, 2, 8, true>,
+constexpr bool kFwdTwoPerCu = (DA + DB <= 192) || (DA == 128 && DB == 128);
+template <int DA, int DB>
+using FwdCfg = typename std::conditional<(DA + DB <= 256), FwdTraits<DA, DB, 2, kFwdTwoPerCu<DA, DB> ? 2 : 1, 8, true>,
                                          FwdTraits<DA, DB, 2, 1, 4, true>>::type;
 
 // Causal heads with few 256-row blocks (the launcher's rule): four waves in

@@ -120,6 +120,13 @@ def test_fullsize_mid_noncausal(gpu_lib):
     _run_full(gpu_lib, "mid", False, full_stats_ok=True)
 
 
+def test_fullsize_mid_causal(gpu_lib):
+    """The mid workload with the causal mask: 32 heads of 16384 rows make 2048
+    workgroups of 256 rows, so this runs the eight-wave causal forward and the
+    dQ/dK kernels at the shape the benchmark times."""
+    _run_full(gpu_lib, "mid", True, full_stats_ok=True)
+
+
 def test_fullsize_long_causal(gpu_lib):
     _run_full(gpu_lib, "long", True, full_stats_ok=False)
 

@@ -129,6 +129,35 @@ def test_workload_structures_reduced(gpu_lib, name, over, causal):
     run_case(gpu_lib, inputs.make(name, **over), causal, 0)
 
 
+def test_causal_eight_wave_forward_reduced(gpu_lib):
+    """1024 heads of 256 rows: B*H*ceil(N_Q/256) = 1024 workgroups, enough that
+    the causal forward takes its eight-wave, 256-row configuration (the one the
+    full causal mid workload runs) rather than the four-wave one for small
+    grids. Every row of four heads against the oracle, and the four-wave
+    configuration (two heads, same values) must agree with it."""
+    import torch
+    d = inputs.make("mid", H=1024, n_q=256, n_k=256)
+    w = d["w"]
+    q1, k1, q2, k2 = upload(d)
+    g = to_gpu_f32(d["g"])
+    kl, l1, l2 = gpu_lib.fwd(q1, k1, q2, k2, w.s1, w.s2, True, 0)
+    _, _, dq2, dk2 = gpu_lib.bwd(q1, k1, q2, k2, kl, l1, l2, g, w.s1, w.s2, True, 0, want=("dq2", "dk2"))
+    small = gpu_lib.fwd(q1[:, :2].contiguous(), k1[:, :2].contiguous(), q2[:, :2].contiguous(),
+                        k2[:, :2].contiguous(), w.s1, w.s2, True, 0)
+    torch.cuda.synchronize()
+    for h in (0, 1, 517, 1023):
+        sl = lambda x: x[:, h:h + 1]  # noqa: E731
+        ref = oracle.backward(sl(d["Q1"]), sl(d["K1"]), sl(d["Q2"]), sl(d["K2"]), w.s1, w.s2, True, 0,
+                              sl(d["g"]))
+        check_rows("kl", kl[:, h:h + 1].cpu().numpy(), ref[0])
+        check_rows("lse1", l1[:, h:h + 1].cpu().numpy(), ref[1])
+        check_rows("lse2", l2[:, h:h + 1].cpu().numpy(), ref[2])
+        check_grad("dq2", dq2[:, h:h + 1].cpu().numpy(), ref[5])
+        check_grad("dk2", dk2[:, h:h + 1].cpu().numpy(), ref[6])
+    for a, b in zip(small, (kl, l1, l2)):
+        assert torch.allclose(a, b[:, :2], rtol=1e-5, atol=1e-5)
+
+
 def test_deterministic_and_inputs_untouched(gpu_lib):
     import torch
     d = inputs.make("distill", H=2, n_q=384, n_k=384)

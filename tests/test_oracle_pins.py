@@ -365,11 +365,32 @@ def test_acc_invariant_after_each_tile():
     q1, k1, q2, k2 = (d[k][0, 0].astype(np.float64) for k in ("Q1", "K1", "Q2", "K2"))
     S1, S2 = om._logits(q1, k1, q2, k2, w.s1, w.s2)
     mask = np.ones_like(S1, dtype=bool)
-    st = om._init_state(16)
+    st = om.empty_state(16)
     for j0 in range(0, 64, 8):
-        st = om._update(st, S1[:, j0:j0 + 8], S2[:, j0:j0 + 8], mask[:, j0:j0 + 8])
+        st = om.merge_states(st, om.tile_state(S1[:, j0:j0 + 8], S2[:, j0:j0 + 8], mask[:, j0:j0 + 8]))
         seen = slice(0, j0 + 8)
         m1 = S1[:, seen].max(axis=1)
         np.testing.assert_allclose(st["m1"], m1, rtol=0, atol=0)
         ref = (np.exp(S1[:, seen] - m1[:, None]) * (S1[:, seen] - S2[:, seen])).sum(axis=1)
         np.testing.assert_allclose(st["acc"], ref, rtol=1e-12, atol=1e-13)
+
+
+def test_empty_partial_state_is_neutral():
+    """A set of keys a row may not see gives the empty state, and merging it
+    changes nothing: a causal row's tiles past its frontier, and a split-K
+    chunk that holds none of its keys."""
+    from oracle import online_model as om
+    rng = np.random.default_rng(5)
+    S1, S2 = rng.standard_normal((4, 6)), rng.standard_normal((4, 6))
+    mask = np.ones((4, 6), dtype=bool)
+    mask[1] = False           # row 1 sees none of these keys
+    mask[2, 3:] = False
+    t = om.tile_state(S1, S2, mask)
+    assert np.isneginf(t["m1"][1]) and np.isneginf(t["m2"][1])
+    assert t["l1"][1] == 0.0 and t["l2"][1] == 0.0 and t["acc"][1] == 0.0
+    full = om.tile_state(S1, S2, np.ones((4, 6), dtype=bool))
+    for a, b in ((om.merge_states(full, om.empty_state(4)), full), (om.merge_states(om.empty_state(4), full), full)):
+        for k in full:
+            np.testing.assert_array_equal(a[k], b[k])
+    kl, l1, l2 = om.finalize(om.empty_state(3))
+    assert np.all(kl == 0.0) and np.all(np.isneginf(l1)) and np.all(np.isneginf(l2))
