@@ -59,7 +59,8 @@ typedef enum {
   STREAMKL_OK = 0,
   STREAMKL_ERR_INVALID_ARG = 1, /* NULL pointer, negative extent, bad flag, scale, alignment */
   STREAMKL_ERR_UNSUPPORTED = 2, /* head dim outside {64, 128, 192, 256}, extent too large  */
-  STREAMKL_ERR_HIP = 3          /* a kernel launch was rejected by the HIP runtime          */
+  STREAMKL_ERR_HIP = 3,         /* a kernel launch was rejected by the HIP runtime          */
+  STREAMKL_ERR_SCRATCH_LIMIT = 4 /* streamkl_fwd_split_noalloc: partials exceed its scratch */
 } streamkl_status;
 
 typedef enum {
@@ -187,6 +188,36 @@ int streamkl_fwd_split(const void* Q1, const void* K1, const void* Q2, const voi
                        void* workspace, size_t workspace_bytes,
                        float* kl, float* lse1, float* lse2,
                        hipStream_t stream);
+
+/* Bytes of device memory streamkl_fwd_split_noalloc holds on each GPU it runs on. */
+#define STREAMKL_NOALLOC_SCRATCH_BYTES (16u << 20)
+
+/*
+ * Allocation-free split-K forward, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc. Arguments, outputs and results are those of
+ * streamkl_fwd_split without the workspace: the partial row statistics go to
+ * a static array of STREAMKL_NOALLOC_SCRATCH_BYTES (16 MiB) that the library
+ * holds on every GPU it runs on until the process ends. The call allocates
+ * and frees nothing.
+ *   - A request whose partials need more
+ *     (streamkl_fwd_split_workspace_bytes(B, H, N_Q, splits) >
+ *     STREAMKL_NOALLOC_SCRATCH_BYTES) returns STREAMKL_ERR_SCRATCH_LIMIT and
+ *     launches nothing; splits = 1 needs no scratch.
+ *   - Every call on one GPU uses that GPU's one array, which keeps the last
+ *     call's contents. Calls whose work may overlap on one GPU (different
+ *     streams, or host threads without ordering between them) race on it and
+ *     give undefined results; calls ordered on one stream are safe. Nothing
+ *     in it needs clearing: every partial is written before it is read.
+ *   - `stream` must belong to the current device (else
+ *     STREAMKL_ERR_INVALID_ARG). The first call on a device looks up the
+ *     array's address there; if HIP fails that lookup, STREAMKL_ERR_HIP.
+ */
+int streamkl_fwd_split_noalloc(const void* Q1, const void* K1, const void* Q2, const void* K2,
+                               int B, int H, int N_Q, int N_K, int d1, int d2,
+                               float s1, float s2, int causal, int direction, int splits,
+                               float* kl, float* lse1, float* lse2,
+                               hipStream_t stream);
 
 /* Workspace bytes streamkl_fwd_split needs: 20 * splits * B * H * N_Q when
    splits > 1, else 0. Returns 0 for negative extents. */

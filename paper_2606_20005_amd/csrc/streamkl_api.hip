@@ -2,6 +2,7 @@
 // KL direction into (first slot, second slot) roles, and kernel dispatch.
 // Every check happens before anything is enqueued, and no HIP call is made
 // on an error path, so the checks are exercised on hosts without a GPU.
+#include <atomic>
 #include <cmath>
 #include <cstdint>
 
@@ -65,11 +66,45 @@ hipError_t zero_fill(float* p, size_t n, hipStream_t stream) {
 
 }  // namespace
 
+// ---------------------------------------------------------------------------
+// Static scratch of the allocation-free split-K forward
+// (streamkl_fwd_split_noalloc): the five partial row statistics of every
+// (chunk, row), in the layout the split-K kernels use for a caller's
+// workspace. Every GPU the library runs on holds its own copy for the life of
+// the process. In host code `scratch` only names the variable: its device
+// address on a GPU comes from hipGetSymbolAddress with that GPU current, once
+// per device, and only that address is ever handed to a kernel.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) float scratch[STREAMKL_NOALLOC_SCRATCH_BYTES / sizeof(float)];
+
 namespace {
 
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_addr[kMaxDevices];
+
+// Device address of the scratch array on the device of `stream`, which must
+// be the current device. The first call on a device looks it up; concurrent
+// first calls look up the same address, so the race is benign.
+int scratch_address(hipStream_t stream, void** out) {
+  int cur = -1;
+  hipDevice_t sdev = -1;
+  if (hipGetDevice(&cur) != hipSuccess || hipStreamGetDevice(stream, &sdev) != hipSuccess) return STREAMKL_ERR_HIP;
+  if (sdev != cur) return STREAMKL_ERR_INVALID_ARG;
+  if (cur < 0 || cur >= kMaxDevices) return STREAMKL_ERR_UNSUPPORTED;
+  void* p = g_scratch_addr[cur].load(std::memory_order_acquire);
+  if (!p) {
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return STREAMKL_ERR_HIP;
+    g_scratch_addr[cur].store(p, std::memory_order_release);
+  }
+  *out = p;
+  return STREAMKL_OK;
+}
+
+// use_scratch: the partials of a split-K call go to the static scratch array
+// (workspace and workspace_bytes are ignored).
 int fwd_common(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H, int N_Q, int N_K, int d1,
                int d2, float s1, float s2, int causal, int direction, int splits, void* workspace,
-               size_t workspace_bytes, float* kl, float* lse1, float* lse2, hipStream_t stream) {
+               size_t workspace_bytes, bool use_scratch, float* kl, float* lse1, float* lse2, hipStream_t stream) {
   bool empty = false;
   const int st = check_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, &empty);
   if (st != STREAMKL_OK) return st;
@@ -81,13 +116,20 @@ int fwd_common(const void* Q1, const void* K1, const void* Q2, const void* K2, i
     const long long merge_grid =
         (rows + streamkl::fwd_merge_rows_per_workgroup() - 1) / streamkl::fwd_merge_rows_per_workgroup();
     if (grid > kMaxGrid || merge_grid > kMaxGrid || rows * splits > (1LL << 40)) return STREAMKL_ERR_UNSUPPORTED;
-    if (!empty && (!workspace || !aligned(workspace, 4) ||
-                   workspace_bytes < streamkl_fwd_split_workspace_bytes(B, H, N_Q, splits)))
+    const size_t need = streamkl_fwd_split_workspace_bytes(B, H, N_Q, splits);
+    if (use_scratch) {
+      if (need > STREAMKL_NOALLOC_SCRATCH_BYTES) return STREAMKL_ERR_SCRATCH_LIMIT;
+    } else if (!empty && (!workspace || !aligned(workspace, 4) || workspace_bytes < need)) {
       return STREAMKL_ERR_INVALID_ARG;
+    }
   }
   if (empty) return STREAMKL_OK;
   if (!kl || !lse1 || !lse2) return STREAMKL_ERR_INVALID_ARG;
   if (!aligned(kl, 4) || !aligned(lse1, 4) || !aligned(lse2, 4)) return STREAMKL_ERR_INVALID_ARG;
+  if (use_scratch && splits > 1) {
+    const int sst = scratch_address(stream, &workspace);
+    if (sst != STREAMKL_OK) return sst;
+  }
   const bool rev = direction == STREAMKL_KL_REV;
   FwdArgs a;
   a.Qa = static_cast<const uint16_t*>(rev ? Q2 : Q1);
@@ -112,8 +154,8 @@ int fwd_common(const void* Q1, const void* K1, const void* Q2, const void* K2, i
 extern "C" int streamkl_fwd(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H, int N_Q,
                             int N_K, int d1, int d2, float s1, float s2, int causal, int direction, float* kl,
                             float* lse1, float* lse2, hipStream_t stream) {
-  return fwd_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, 1, nullptr, 0, kl, lse1,
-                    lse2, stream);
+  return fwd_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, 1, nullptr, 0, false, kl,
+                    lse1, lse2, stream);
 }
 
 extern "C" int streamkl_fwd_split(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H,
@@ -121,7 +163,15 @@ extern "C" int streamkl_fwd_split(const void* Q1, const void* K1, const void* Q2
                                   int splits, void* workspace, size_t workspace_bytes, float* kl, float* lse1,
                                   float* lse2, hipStream_t stream) {
   return fwd_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, splits, workspace,
-                    workspace_bytes, kl, lse1, lse2, stream);
+                    workspace_bytes, false, kl, lse1, lse2, stream);
+}
+
+extern "C" int streamkl_fwd_split_noalloc(const void* Q1, const void* K1, const void* Q2, const void* K2, int B,
+                                          int H, int N_Q, int N_K, int d1, int d2, float s1, float s2, int causal,
+                                          int direction, int splits, float* kl, float* lse1, float* lse2,
+                                          hipStream_t stream) {
+  return fwd_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, splits, nullptr, 0, true, kl,
+                    lse1, lse2, stream);
 }
 
 extern "C" size_t streamkl_fwd_split_workspace_bytes(int B, int H, int N_Q, int splits) {
@@ -272,6 +322,8 @@ extern "C" const char* streamkl_strerror(int status) {
     case STREAMKL_ERR_INVALID_ARG: return "invalid argument (null pointer, negative extent, flag, scale or alignment)";
     case STREAMKL_ERR_UNSUPPORTED: return "unsupported configuration (head dim not in {64,128,192,256} or extent too large)";
     case STREAMKL_ERR_HIP: return "HIP runtime rejected a kernel launch";
+    case STREAMKL_ERR_SCRATCH_LIMIT:
+      return "request needs more partial-statistics space than the allocation-free forward's static scratch holds";
     default: return "unknown status";
   }
 }

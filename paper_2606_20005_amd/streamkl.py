@@ -20,13 +20,14 @@ import torch
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libstreamkl.so")
 
-OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP = 0, 1, 2, 3
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_HIP, ERR_SCRATCH_LIMIT = 0, 1, 2, 3, 4
+NOALLOC_SCRATCH_BYTES = 16 << 20
 FWD, REV = 0, 1
 BWD_AUTO, BWD_SEPARATE, BWD_FUSED = 0, 1, 2
 GRAD_BITS = {"dq1": 1, "dk1": 2, "dq2": 4, "dk2": 8}
 ENTRY_POINTS = ("streamkl_fwd", "streamkl_bwd", "streamkl_bwd_ex", "streamkl_bwd_choose", "streamkl_fwd_split",
-                "streamkl_fwd_split_workspace_bytes", "streamkl_fwd_split_count", "streamkl_strerror",
-                "streamkl_version", "streamkl_supported_head_dim")
+                "streamkl_fwd_split_noalloc", "streamkl_fwd_split_workspace_bytes", "streamkl_fwd_split_count",
+                "streamkl_strerror", "streamkl_version", "streamkl_supported_head_dim")
 
 
 def _load():
@@ -47,6 +48,8 @@ def _load():
     sz = ctypes.c_size_t
     lib.streamkl_fwd_split.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, f, f, i, i, i, vp, sz, vp, vp, vp, vp]
     lib.streamkl_fwd_split.restype = i
+    lib.streamkl_fwd_split_noalloc.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, f, f, i, i, i, vp, vp, vp, vp]
+    lib.streamkl_fwd_split_noalloc.restype = i
     lib.streamkl_fwd_split_workspace_bytes.argtypes = [i, i, i, i]
     lib.streamkl_fwd_split_workspace_bytes.restype = sz
     lib.streamkl_fwd_split_count.argtypes = [i, i, i, i, i, i]
@@ -178,6 +181,27 @@ def fwd_split(q1, k1, q2, k2, s1=None, s2=None, causal=False, direction=FWD, spl
                                     _p(kl), _p(lse1), _p(lse2), _stream(dev))
     if st != OK:
         raise StreamKLError(st, "streamkl_fwd_split")
+    return kl, lse1, lse2
+
+
+def fwd_split_noalloc(q1, k1, q2, k2, s1=None, s2=None, causal=False, direction=FWD, splits="auto", out=None):
+    """streamkl_fwd_split_noalloc: the split-K forward with its partial row
+    statistics in the library's static per-GPU scratch (nothing is allocated
+    for them); returns (kl, lse1, lse2) like fwd_split. Outputs are allocated
+    here unless ``out`` is given."""
+    B, H, NQ, NK, d1, d2 = _check_inputs(q1, k1, q2, k2)
+    s1, s2 = _scales(s1, s2, d1, d2)
+    dev = q1.device
+    w = split_count(B, H, NQ, NK, d1, d2) if splits == "auto" else int(splits)
+    if out is None:
+        out = tuple(torch.empty((B, H, NQ), dtype=torch.float32, device=dev) for _ in range(3))
+    kl, lse1, lse2 = (_f32_rows(t, (B, H, NQ), dev, n) for t, n in zip(out, ("kl", "lse1", "lse2")))
+    with torch.cuda.device(dev):
+        st = lib.streamkl_fwd_split_noalloc(_p(q1), _p(k1), _p(q2), _p(k2), B, H, NQ, NK, d1, d2, s1, s2,
+                                            int(bool(causal)), _direction(direction), w, _p(kl), _p(lse1),
+                                            _p(lse2), _stream(dev))
+    if st != OK:
+        raise StreamKLError(st, "streamkl_fwd_split_noalloc")
     return kl, lse1, lse2
 
 

@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol(sk):
 
 def test_version_and_strerror(sk):
     assert sk.version().startswith("streamkl ") and "gfx950" in sk.version()
-    for st in range(4):
+    for st in range(5):
         assert sk.lib.streamkl_strerror(st)
     assert b"unknown" in sk.lib.streamkl_strerror(99)
     assert [d for d in range(0, 300) if sk.supported_head_dim(d)] == [64, 128, 192, 256]
@@ -211,3 +211,32 @@ def test_split_merge_grid_limit(sk):
     assert split_call(sk, **big) == 2
     # 2^31 rows pass the grid checks and stop at the next one (no output pointer): nothing is launched
     assert split_call(sk, **dict(big, B=128, kl=None)) == 1
+
+
+def noalloc_call(sk, **kw):
+    a = dict(Q1=FAKE, K1=FAKE, Q2=FAKE, K2=FAKE, B=16, H=1, NQ=64, NK=65536, d1=128, d2=128, s1=0.125, s2=0.125,
+             causal=0, direction=0, splits=32, kl=FAKE, lse1=FAKE, lse2=FAKE, stream=None)
+    a.update(kw)
+    return sk.lib.streamkl_fwd_split_noalloc(a["Q1"], a["K1"], a["Q2"], a["K2"], a["B"], a["H"], a["NQ"], a["NK"],
+                                             a["d1"], a["d2"], a["s1"], a["s2"], a["causal"], a["direction"],
+                                             a["splits"], a["kl"], a["lse1"], a["lse2"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(Q1=None), 1), (dict(kl=None), 1), (dict(splits=0), 1), (dict(causal=3), 1), (dict(d2=96), 2),
+    (dict(B=0), 0), (dict(NQ=0), 0),
+    # partials of 20 * W * B * H * N_Q bytes must fit the static scratch
+    (dict(NQ=8192, splits=32), 4), (dict(B=1, NQ=1 << 20, splits=2), 4),
+])
+def test_noalloc_argument_checks(sk, kw, expect):
+    assert noalloc_call(sk, **kw) == expect
+
+
+def test_noalloc_scratch_limit_is_the_header_constant(sk):
+    text = open(HEADER).read()
+    m = re.search(r"#define STREAMKL_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == sk.NOALLOC_SCRATCH_BYTES == 16 << 20
+    # largest W for B*H*N_Q = 1024 rows that still fits: 20 * W * 1024 <= 16 MiB
+    w_max = sk.NOALLOC_SCRATCH_BYTES // (20 * 1024)
+    assert sk.split_workspace_bytes(16, 1, 64, w_max) <= sk.NOALLOC_SCRATCH_BYTES
+    assert noalloc_call(sk, splits=w_max + 1) == sk.ERR_SCRATCH_LIMIT
