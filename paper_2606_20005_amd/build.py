@@ -22,6 +22,9 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(ROOT, "_build", "obj")
 LIB = os.path.join(PKG, "libstreamkl.so")
+# benchmark-only kernels (measured MFMA peak), kept out of the library's ABI
+BENCH_SRC = os.path.join(CSRC, "bench")
+BENCH_LIB = os.path.join(PKG, "libstreamkl_bench.so")
 ARCH = "gfx950"
 
 CFLAGS = [
@@ -52,21 +55,28 @@ def _run(cmd, verbose):
 
 
 def build(jobs: int | None = None, verbose: bool = False) -> str:
-    """Compile every csrc/*.hip for gfx950 and link libstreamkl.so; returns its path."""
+    """Compile every csrc/*.hip for gfx950 and link libstreamkl.so (and the benchmark kernels under
+    csrc/bench/ into libstreamkl_bench.so); returns the library's path."""
     cc = hipcc()
     os.makedirs(OBJDIR, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+    bench_srcs = sorted(glob.glob(os.path.join(BENCH_SRC, "*.hip")))
     if not srcs:
         raise RuntimeError(f"no sources under {CSRC}")
-    objs = [os.path.join(OBJDIR, os.path.basename(s)[:-4] + ".o") for s in srcs]
-    jobs = jobs or min(len(srcs), max(1, min(16, os.cpu_count() or 1)))
+    allsrc = srcs + bench_srcs
+    objs = [os.path.join(OBJDIR, ("bench_" if s in bench_srcs else "") + os.path.basename(s)[:-4] + ".o")
+            for s in allsrc]
+    jobs = jobs or min(len(allsrc), max(1, min(16, os.cpu_count() or 1)))
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
-        futs = [ex.submit(_run, [cc, *CFLAGS, "-c", s, "-o", o], verbose) for s, o in zip(srcs, objs)]
+        futs = [ex.submit(_run, [cc, *CFLAGS, "-c", s, "-o", o], verbose) for s, o in zip(allsrc, objs)]
         for f in futs:
             f.result()
-    tmp = LIB + ".tmp"
-    _run([cc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp], verbose)
-    os.replace(tmp, LIB)
+    for lib, part in ((LIB, objs[:len(srcs)]), (BENCH_LIB, objs[len(srcs):])):
+        if not part:
+            continue
+        tmp = lib + ".tmp"
+        _run([cc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *part, "-o", tmp], verbose)
+        os.replace(tmp, lib)
     return LIB
 
 
