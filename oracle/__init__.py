@@ -12,6 +12,9 @@ Modules
 -------
 kl_oracle     the plain definition (Sec. 2.1, eq:kl-def / eq:kl-case1 /
               eq:kl-case2): explicit P1 and P2 row block by row block in fp64.
+sigmoid_oracle  the same divergence under sigmoid attention scores with no
+              normalisation (Sec. 3.1, "Generalizability beyond Softmax"): the
+              generalized KL of the two score rows and its gradients.
 online_model  the online forward (Sec. 3.2) evaluated from per-tile partial
               states folded with the split-K merge of Sec. 3.3, in fp64. It
               is not the oracle; it pins the paper's online derivation
@@ -29,3 +32,4 @@ from .kl_oracle import (  # noqa: F401
     allowed_mask,
 )
 from .online_model import online_forward_head, split_merge_forward_head  # noqa: F401
+from . import sigmoid_oracle  # noqa: F401,E402
