@@ -68,6 +68,12 @@ typedef enum {
   STREAMKL_KL_REV = 1  /* L = KL(P2 || P1), the two roles swapped    */
 } streamkl_direction;
 
+/* Attention-score activations (Sec. 3.1, "Generalizability beyond Softmax"). */
+typedef enum {
+  STREAMKL_ACT_SOFTMAX = 0, /* P_t = softmax(S_t); L = KL(P1 || P2), eq:kl-def                  */
+  STREAMKL_ACT_SIGMOID = 1  /* A_t = sigmoid(S_t), not normalised; L = generalized KL (below)  */
+} streamkl_activation;
+
 /* Backward kernel strategies of Sec. 4.2 ("GPU Kernel Design"). */
 typedef enum {
   STREAMKL_BWD_AUTO = 0,     /* adaptive selection (streamkl_bwd_choose)          */
@@ -162,6 +168,48 @@ int streamkl_bwd_ex(const void* Q1, const void* K1, const void* Q2, const void* 
  */
 int streamkl_bwd_choose(int B, int H, int N_Q, int N_K, int d1, int d2,
                         int causal, int direction, int grads);
+
+/*
+ * Forward with a choice of score activation (Sec. 3.1, "Generalizability
+ * beyond Softmax": activations without softmax's global normalisation need
+ * no normalisers). The paper defines neither the scores nor the divergence
+ * for that case; this library reads it as:
+ *   STREAMKL_ACT_SOFTMAX  exactly streamkl_fwd (stat1, stat2 = lse1, lse2).
+ *   STREAMKL_ACT_SIGMOID  A_t[j] = sigmoid(S_t[j]) with no normalisation and
+ *       L = sum_j [A1 log(A1 / A2) - A1 + A2] over the keys the row may
+ *       attend (the generalized KL divergence of the two score rows: >= 0,
+ *       0 iff A1 = A2, eq:kl-def when both rows sum to 1); REV swaps the
+ *       roles. stat1, stat2 receive the row masses sum_j A1[j], sum_j A2[j]
+ *       (each may be NULL). A row with no visible key gives L = 0. ReLU and
+ *       tanh scores are not offered: under this divergence L is infinite
+ *       where A2 = 0 < A1 (ReLU) and undefined for negative scores (tanh).
+ * Single pass only (no split-K); other arguments, layouts and errors as for
+ * streamkl_fwd. An activation outside the enum is STREAMKL_ERR_INVALID_ARG.
+ */
+int streamkl_fwd_act(const void* Q1, const void* K1, const void* Q2, const void* K2,
+                     int B, int H, int N_Q, int N_K, int d1, int d2,
+                     float s1, float s2, int causal, int direction, int activation,
+                     float* kl, float* stat1, float* stat2,
+                     hipStream_t stream);
+
+/*
+ * Backward for streamkl_fwd_act's objective sum_{b,h,i} dkl L (separate
+ * query- and key-owned kernels; bitwise reproducible).
+ *   STREAMKL_ACT_SOFTMAX  exactly streamkl_bwd (kl, stat1, stat2 = kl, lse1,
+ *                         lse2 of the forward).
+ *   STREAMKL_ACT_SIGMOID  FWD: dS2 = g (A2 - A1)(1 - A2),
+ *                              dS1 = g A1 (1 - A1)(log A1 - log A2);
+ *                         REV: the roles swapped. No saved statistic is
+ *                         needed: kl, stat1, stat2 are not read (may be NULL).
+ * dQ_t = s_t dS_t K_t, dK_t = s_t dS_t^T Q_t; other arguments as streamkl_bwd.
+ */
+int streamkl_bwd_act(const void* Q1, const void* K1, const void* Q2, const void* K2,
+                     int B, int H, int N_Q, int N_K, int d1, int d2,
+                     float s1, float s2, int causal, int direction, int activation,
+                     const float* kl, const float* stat1, const float* stat2,
+                     const float* dkl,
+                     float* dQ1, float* dK1, float* dQ2, float* dK2,
+                     hipStream_t stream);
 
 /*
  * Split-K forward (Sec. 3.3, "Split-K variant" and "Adaptive split

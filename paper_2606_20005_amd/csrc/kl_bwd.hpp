@@ -27,6 +27,14 @@
 
 namespace streamkl {
 
+// Activation of the attention scores: softmax (the paper's method) or the
+// unnormalised sigmoid of Sec. 3.1 (see SigmoidRows in kl_fwd.hpp). With
+// sigmoid scores A = sigmoid(S) the logit gradients of g L need no saved row
+// statistic:  dS_b = g (A_b - A_a)(1 - A_b),
+//             dS_a = g A_a (1 - A_a)(log A_a - log A_b).
+constexpr int kActSoftmax = 0;
+constexpr int kActSigmoid = 1;
+
 template <int DA, int DB, int MODE>
 struct BwdCfg {
   static constexpr int NW = 4;
@@ -89,24 +97,29 @@ __device__ __forceinline__ RowStats load_row_stats(const float* kl, const float*
 // the dK kernel loads them one tile ahead). Once they have landed,
 // stage_row_stats turns the 32 rows of a tile into the form the inner loop
 // uses.
+// (Sigmoid scores need g alone: ACT = kActSigmoid issues only that load, and
+// the statistics pointers, which the caller may leave null, are not used.)
 struct RowsDma {
   rsrc_t r_la, r_lb, r_kl, r_g;
   bool has_g;
   __device__ __forceinline__ RowsDma(const float* kl, const float* lse_a, const float* lse_b, const float* g,
                                      size_t head_row0, int NQ) {
     const uint32_t bytes = (uint32_t)NQ * 4u;
-    r_la = make_rsrc(lse_a + head_row0, bytes);
-    r_lb = make_rsrc(lse_b + head_row0, bytes);
-    r_kl = make_rsrc(kl + head_row0, bytes);
     has_g = g != nullptr;
-    r_g = make_rsrc(has_g ? g + head_row0 : kl + head_row0, bytes);
+    r_g = make_rsrc(has_g ? g + head_row0 : g, has_g ? bytes : 0u);
+    r_la = make_rsrc(lse_a ? lse_a + head_row0 : lse_a, lse_a ? bytes : 0u);
+    r_lb = make_rsrc(lse_b ? lse_b + head_row0 : lse_b, lse_b ? bytes : 0u);
+    r_kl = make_rsrc(kl ? kl + head_row0 : kl, kl ? bytes : 0u);
   }
+  template <int ACT>
   __device__ __forceinline__ void issue(int row0, float (*raw)[64], int lane) const {
 #if defined(__HIP_DEVICE_COMPILE__)
     const uint32_t off = (uint32_t)(row0 + lane) * 4u;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r_la, (lds_void*)raw[0], 4, off, 0, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r_lb, (lds_void*)raw[1], 4, off, 0, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r_kl, (lds_void*)raw[2], 4, off, 0, 0, 0);
+    if constexpr (ACT == kActSoftmax) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r_la, (lds_void*)raw[0], 4, off, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r_lb, (lds_void*)raw[1], 4, off, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(r_kl, (lds_void*)raw[2], 4, off, 0, 0, 0);
+    }
     if (has_g) __builtin_amdgcn_raw_ptr_buffer_load_lds(r_g, (lds_void*)raw[3], 4, off, 0, 0, 0);
 #endif
   }
@@ -116,9 +129,17 @@ struct RowsDma {
 // in *fold whether g has been folded into lsa2, lsb2 (every g of the tile
 // >= 0, the usual case; the stored g is then 1): the tile loop may then skip
 // one multiply per distribution and element. Rows at tid >= BS idle.
-template <int BS>
+template <int BS, int ACT = kActSoftmax>
 __device__ __forceinline__ void stage_row_stats(const float (*raw)[64], int r0, int NQ, bool has_g,
                                                 f32x4 (&dst)[4][BS / 4], int* fold, int tid) {
+  if constexpr (ACT == kActSigmoid) {   // g alone, never folded
+    if (tid < BS) {
+      float* p = reinterpret_cast<float*>(&dst[0][0]);
+      p[2 * BS + tid] = r0 + tid < NQ ? (has_g ? raw[3][tid] : 1.f) : 0.f;
+      if (tid == 0) *fold = 0;
+    }
+    return;
+  }
   RowStats s{0.f, 0.f, 0.f, 0.f};
   if (tid < BS) {
     const float la = raw[0][tid];
@@ -149,9 +170,17 @@ __device__ __forceinline__ void stage_row_stats(const float (*raw)[64], int r0, 
 // |g| is already folded into the exponent offsets (lsa2, lsb2 lowered by
 // log2 |g|), so the exponentials are g P directly and the sign of g is
 // applied elsewhere; otherwise g multiplies here.
-template <bool WANT_A, bool WANT_B, bool FOLD = false>
+template <bool WANT_A, bool WANT_B, bool FOLD = false, int ACT = kActSoftmax>
 __device__ __forceinline__ void dlogits(float ra, float rb, bool ok, float ca, float cb, float sa, float sb,
                                         const RowStats& s, float& dsa, float& dsb) {
+  if constexpr (ACT == kActSigmoid) {
+    // ca, cb = s * log2(e): sigmoid_terms takes the logit in base-2 units;
+    // nl_b - nl_a = log2 A_a - log2 A_b
+    const SigmoidTerms ta = sigmoid_terms(ra * ca), tb = sigmoid_terms(rb * cb);
+    if constexpr (WANT_B) dsb = ok ? s.g * ((tb.a - ta.a) * tb.na) : 0.f;
+    if constexpr (WANT_A) dsa = ok ? s.g * (ta.a * ta.na) * ((tb.nl - ta.nl) * kLn2) : 0.f;
+    return;
+  }
   const float xa = ok ? __builtin_fmaf(ra, ca, -s.lsa2) : kNegInf;
   const float pa = exp2_fast(xa);
   if constexpr (WANT_B) {
@@ -191,7 +220,7 @@ __device__ __forceinline__ void mfma_phase_end() {
 // allowed pair.
 // ----------------------------------------------------------------------------
 // ra_op(ks), rb_op(ks) return the resident operands of k-step ks (16 columns).
-template <int DA, int DB, int MODE, bool MASK, bool FOLD, typename OpA, typename OpB, typename StatsFn,
+template <int DA, int DB, int MODE, bool MASK, bool FOLD, int ACT, typename OpA, typename OpB, typename StatsFn,
           typename OkFn>
 __device__ __forceinline__ void bwd_dlogits_tile(const u32x4* stage, OpA ra_op, OpB rb_op, float ca, float cb,
                                                  float sa, float sb, int lane, StatsFn stats, OkFn ok,
@@ -211,7 +240,8 @@ __device__ __forceinline__ void bwd_dlogits_tile(const u32x4* stage, OpA ra_op, 
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     const RowStats rs = stats(i);
-    dlogits<C::WANT_A, C::WANT_B, FOLD>(s_a[i], s_b[i], MASK ? ok(i) : true, ca, cb, sa, sb, rs, dsa[i], dsb[i]);
+    dlogits<C::WANT_A, C::WANT_B, FOLD, ACT>(s_a[i], s_b[i], MASK ? ok(i) : true, ca, cb, sa, sb, rs, dsa[i],
+                                             dsb[i]);
   }
 }
 
@@ -290,7 +320,7 @@ __device__ __forceinline__ void bwd_grad_tile(const u32x4* stage, const float (&
   mfma_phase_end<MODE>();
 }
 
-template <int DA, int DB, int MODE, bool MASK, bool FOLD, typename StatsFn, typename OkFn>
+template <int DA, int DB, int MODE, bool MASK, bool FOLD, int ACT = kActSoftmax, typename StatsFn, typename OkFn>
 __device__ __forceinline__ void bwd_tile(const u32x4* stage, const bf16x8 (&ra_op)[DA / 16],
                                          const bf16x8 (&rb_op)[DB / 16],
                                          f32x16 (&ga)[(MODE & 2) ? DA / 32 : 1],
@@ -298,7 +328,7 @@ __device__ __forceinline__ void bwd_tile(const u32x4* stage, const bf16x8 (&ra_o
                                          float ca, float cb, float sa, float sb, int lane,
                                          StatsFn stats, OkFn ok, const TrOffsets<DA, DB, MODE>& to) {
   float dsa[16], dsb[16];
-  bwd_dlogits_tile<DA, DB, MODE, MASK, FOLD>(stage, [&](int ks) { return ra_op[ks]; },
+  bwd_dlogits_tile<DA, DB, MODE, MASK, FOLD, ACT>(stage, [&](int ks) { return ra_op[ks]; },
                                              [&](int ks) { return rb_op[ks]; }, ca, cb, sa, sb, lane, stats, ok,
                                              dsa, dsb);
   bwd_grad_tile<DA, DB, MODE>(stage, dsa, dsb, ga, gb, to);
@@ -342,7 +372,7 @@ __device__ __forceinline__ void write_grad(float* out, const f32x16 (&acc)[D / 3
 // ----------------------------------------------------------------------------
 // dQ kernel: workgroup = 128 query rows of one (batch, head), streams key tiles.
 // ----------------------------------------------------------------------------
-template <int DA, int DB, bool CAUSAL, int MODE>
+template <int DA, int DB, bool CAUSAL, int MODE, int ACT = kActSoftmax>
 __global__ void __launch_bounds__(kThreads, (BwdCfg<DA, DB, MODE>::MINB))
 kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
                  const uint16_t* __restrict__ Qb, const uint16_t* __restrict__ Kb,
@@ -379,9 +409,15 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
 
   // |g| of the lane's row goes into its exponent offsets, its sign into the
   // written row
-  const RowStats rs0 = load_row_stats(kl, lse_a, lse_b, g, (size_t)bh * NQ + myq, myq < NQ);
-  const float gsign = rs0.g < 0.f ? -1.f : 1.f;
-  const RowStats rs = fold_row_stats(rs0);
+  // (sigmoid scores: only g, applied in the tile; kl and the LSEs are not read)
+  constexpr bool FOLD = ACT == kActSoftmax;
+  RowStats rs0{0.f, 0.f, 0.f, 0.f};
+  if constexpr (ACT == kActSoftmax)
+    rs0 = load_row_stats(kl, lse_a, lse_b, g, (size_t)bh * NQ + myq, myq < NQ);
+  else if (myq < NQ)
+    rs0.g = g ? g[(size_t)bh * NQ + myq] : 1.f;
+  const float gsign = FOLD && rs0.g < 0.f ? -1.f : 1.f;
+  const RowStats rs = FOLD ? fold_row_stats(rs0) : rs0;
   bf16x8 qa[DA / 16], qb[DB / 16];
   load_resident<DA>(qa, Qa, (size_t)bh * NQ, myq, NQ, half);
   load_resident<DB>(qb, Qb, (size_t)bh * NQ, myq, NQ, half);
@@ -416,9 +452,9 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
       return k < NK && k <= kmax_ok;
     };
     if (opaque(need_mask))
-      bwd_tile<DA, DB, MODE, true, true>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, lane, stats, ok, tro);
+      bwd_tile<DA, DB, MODE, true, FOLD, ACT>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, lane, stats, ok, tro);
     else
-      bwd_tile<DA, DB, MODE, false, true>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, lane, stats, ok, tro);
+      bwd_tile<DA, DB, MODE, false, FOLD, ACT>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, lane, stats, ok, tro);
   };
 
   if (ntiles > 0) dma.issue(rka, rkb, 0, st0, wave);
@@ -450,7 +486,7 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
 // dK kernel: workgroup = 128 key rows of one (batch, head), streams query tiles
 // together with their row statistics.
 // ----------------------------------------------------------------------------
-template <int DA, int DB, bool CAUSAL, int MODE>
+template <int DA, int DB, bool CAUSAL, int MODE, int ACT = kActSoftmax>
 __global__ void __launch_bounds__(kThreads, (BwdCfg<DA, DB, MODE>::MINB))
 kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
                  const uint16_t* __restrict__ Qb, const uint16_t* __restrict__ Kb,
@@ -529,23 +565,29 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
     };
     // the general path also takes the tiles whose g could not be folded
     // (a third variant would cost registers everywhere)
-    if (opaque(need_mask || !sfold[buf]))
+    if constexpr (ACT == kActSigmoid) {
+      if (opaque(need_mask))
+        bwd_tile<DA, DB, MODE, true, false, ACT>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, lane, stats, ok, tro);
+      else
+        bwd_tile<DA, DB, MODE, false, false, ACT>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, lane, stats, ok, tro);
+    } else if (opaque(need_mask || !sfold[buf])) {
       bwd_tile<DA, DB, MODE, true, false>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, lane, stats, ok, tro);
-    else
+    } else {
       bwd_tile<DA, DB, MODE, false, true>(stage, ka, kb, dka, dkb, ca, cb, sa, sb, lane, stats, ok, tro);
+    }
   };
 
   // The row values of tile t + 1 are turned into statistics by wave 0 early
   // in step t, while the tile is computed: they were loaded with the
   // previous tile, so no wait sits between the end-of-step wait and barrier.
   auto stats_in = [&](int t, float (*raw)[64], int buf) {
-    if (wave == 0) stage_row_stats<C::BS>(raw, t * C::BS, NQ, rdma.has_g, sstat[buf], &sfold[buf], tid);
+    if (wave == 0) stage_row_stats<C::BS, ACT>(raw, t * C::BS, NQ, rdma.has_g, sstat[buf], &sfold[buf], tid);
   };
   if (t_begin < ntq) {
     dma.issue(rqa, rqb, t_begin * C::BS, st0, wave);
     if (wave == 0) {
-      rdma.issue(t_begin * C::BS, sraw0, lane);
-      if (t_begin + 1 < ntq) rdma.issue((t_begin + 1) * C::BS, sraw1, lane);
+      rdma.issue<ACT>(t_begin * C::BS, sraw0, lane);
+      if (t_begin + 1 < ntq) rdma.issue<ACT>((t_begin + 1) * C::BS, sraw1, lane);
     }
     wait_vmem();
     stats_in(t_begin, sraw0, 0);
@@ -554,7 +596,7 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   // rnext holds the row values of tile t + 1; rfree receives those of t + 2
   auto step = [&](const u32x4* cur, u32x4* nxt, float (*rnext)[64], float (*rfree)[64], int t, int buf) {
     if (t + 1 < ntq) dma.issue(rqa, rqb, (t + 1) * C::BS, nxt, wave);
-    if (wave == 0 && t + 2 < ntq) rdma.issue((t + 2) * C::BS, rfree, lane);
+    if (wave == 0 && t + 2 < ntq) rdma.issue<ACT>((t + 2) * C::BS, rfree, lane);
     if (t + 1 < ntq) stats_in(t + 1, rnext, buf ^ 1);
     tile(cur, buf, t);
     wait_vmem();

@@ -1,27 +1,11 @@
-// Instantiations and launcher of the backward dk kernel, gradient mode 3
-// (bit 0: second-slot distribution, bit 1: first-slot distribution).
-#include "kl_bwd.hpp"
-#include "kl_launch.hpp"
+// Instantiations of the key-owned dK backward kernel for gradient mode 3
+// (both distributions), softmax scores.
+#include "kl_bwd_launch.hpp"
 
 namespace streamkl {
 
-template <int DA, int DB, bool CAUSAL>
-static hipError_t run(const BwdArgs& a) {
-  using C = BwdCfg<DA, DB, 3>;
-  const int tiles = (a.NK + C::BR - 1) / C::BR;
-  const dim3 grid((unsigned)((long long)a.BH * tiles));
-  hipLaunchKernelGGL((kl_bwd_dk_kernel<DA, DB, CAUSAL, 3>), grid, dim3(kThreads), 0, a.stream,
-                     a.Qa, a.Ka, a.Qb, a.Kb, a.NQ, a.NK, a.sa, a.sb, a.kl, a.lse_a, a.lse_b, a.g,
-                     a.dKa, a.dKb);
-  return hipGetLastError();
-}
-
 hipError_t launch_bwd_dk_m3(int da, int db, bool causal, const BwdArgs& a) {
-#define STREAMKL_CASE(DA, DB) \
-  if (da == DA && db == DB) return causal ? run<DA, DB, true>(a) : run<DA, DB, false>(a);
-  STREAMKL_FOR_EACH_DIM_PAIR(STREAMKL_CASE)
-#undef STREAMKL_CASE
-  return hipErrorInvalidValue;
+  return launch_bwd_unit<3, kActSoftmax, true>(da, db, causal, a);
 }
 
 }  // namespace streamkl

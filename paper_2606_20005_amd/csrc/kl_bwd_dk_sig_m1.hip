@@ -1,0 +1,11 @@
+// Instantiations of the key-owned dK backward kernel for gradient mode 1
+// (second-slot distribution (Setting 1)), sigmoid scores.
+#include "kl_bwd_launch.hpp"
+
+namespace streamkl {
+
+hipError_t launch_bwd_dk_sig_m1(int da, int db, bool causal, const BwdArgs& a) {
+  return launch_bwd_unit<1, kActSigmoid, true>(da, db, causal, a);
+}
+
+}  // namespace streamkl

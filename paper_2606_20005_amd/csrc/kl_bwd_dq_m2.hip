@@ -1,27 +1,11 @@
-// Instantiations and launcher of the backward dq kernel, gradient mode 2
-// (bit 0: second-slot distribution, bit 1: first-slot distribution).
-#include "kl_bwd.hpp"
-#include "kl_launch.hpp"
+// Instantiations of the query-owned dQ backward kernel for gradient mode 2
+// (first-slot distribution (Setting 2)), softmax scores.
+#include "kl_bwd_launch.hpp"
 
 namespace streamkl {
 
-template <int DA, int DB, bool CAUSAL>
-static hipError_t run(const BwdArgs& a) {
-  using C = BwdCfg<DA, DB, 2>;
-  const int tiles = (a.NQ + C::BR - 1) / C::BR;
-  const dim3 grid((unsigned)((long long)a.BH * tiles));
-  hipLaunchKernelGGL((kl_bwd_dq_kernel<DA, DB, CAUSAL, 2>), grid, dim3(kThreads), 0, a.stream,
-                     a.Qa, a.Ka, a.Qb, a.Kb, a.NQ, a.NK, a.sa, a.sb, a.kl, a.lse_a, a.lse_b, a.g,
-                     a.dQa, a.dQb);
-  return hipGetLastError();
-}
-
 hipError_t launch_bwd_dq_m2(int da, int db, bool causal, const BwdArgs& a) {
-#define STREAMKL_CASE(DA, DB) \
-  if (da == DA && db == DB) return causal ? run<DA, DB, true>(a) : run<DA, DB, false>(a);
-  STREAMKL_FOR_EACH_DIM_PAIR(STREAMKL_CASE)
-#undef STREAMKL_CASE
-  return hipErrorInvalidValue;
+  return launch_bwd_unit<2, kActSoftmax, false>(da, db, causal, a);
 }
 
 }  // namespace streamkl

@@ -251,7 +251,7 @@ kl_bwd_fused_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict_
   const TrOffsets<DA, DB, MODE> tro(lane);
   auto stage_in = [&](int t, u32x4* dst) {
     dma.issue(rqa, rqb, t * C::BS, dst, wave);
-    if (wave == 0) rdma.issue(t * C::BS, reinterpret_cast<float (*)[64]>(dst + BC::STAGE), lane);
+    if (wave == 0) rdma.issue<kActSoftmax>(t * C::BS, reinterpret_cast<float (*)[64]>(dst + BC::STAGE), lane);
   };
 
   // dQ of query tile t from the dS tiles (published by the barrier that ended
@@ -361,9 +361,11 @@ kl_bwd_fused_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict_
     if (active) {
       // the general path also takes the tiles whose g could not be folded
       if (opaque(need_mask || !sfold[buf]))
-        bwd_dlogits_tile<DA, DB, MODE, true, false>(cur, op_a, op_b, ca, cb, sa, sb, ln, stats, ok, dsa, dsb);
+        bwd_dlogits_tile<DA, DB, MODE, true, false, kActSoftmax>(cur, op_a, op_b, ca, cb, sa, sb, ln, stats, ok, dsa,
+                                                                 dsb);
       else
-        bwd_dlogits_tile<DA, DB, MODE, false, true>(cur, op_a, op_b, ca, cb, sa, sb, ln, stats, ok, dsa, dsb);
+        bwd_dlogits_tile<DA, DB, MODE, false, true, kActSoftmax>(cur, op_a, op_b, ca, cb, sa, sb, ln, stats, ok, dsa,
+                                                                 dsb);
     } else {
 #pragma unroll
       for (int e = 0; e < 16; ++e) { dsa[e] = 0.f; dsb[e] = 0.f; }

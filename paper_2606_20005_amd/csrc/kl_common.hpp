@@ -38,6 +38,23 @@ __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const
 // 2^x on the transcendental unit (v_exp_f32); exp2(-inf) = 0.
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// What the sigmoid-score divergence needs of one scaled logit z = S log2(e):
+// a = sigmoid(S), na = 1 - a = sigmoid(-S) and nl = -log2 sigmoid(S) =
+// max(-z, 0) + log2(1 + 2^-|z|), formed from e = 2^-|z| in (0, 1] so that
+// nothing overflows and 1 - a is not a cancellation. A masked stand-in
+// logit (-1e30) gives a = 0, na = 1 and a finite nl.
+struct SigmoidTerms {
+  float a, na, nl;
+};
+__device__ __forceinline__ SigmoidTerms sigmoid_terms(float z) {
+  const float e = __builtin_amdgcn_exp2f(-fabsf(z));
+  const float w = 1.f + e;                          // in (1, 2]
+  const float iw = __builtin_amdgcn_rcpf(w);
+  const float ew = e * iw;
+  const bool pos = z >= 0.f;
+  return SigmoidTerms{pos ? iw : ew, pos ? ew : iw, fmaxf(-z, 0.f) + __builtin_amdgcn_logf(w)};
+}
+
 __device__ __forceinline__ f32x16 zero16() {
   f32x16 z;
 #pragma unroll

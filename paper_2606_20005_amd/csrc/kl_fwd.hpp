@@ -255,6 +255,103 @@ __device__ __forceinline__ void write_row(const RowPartial& p, size_t ri, float*
   lse_b[ri] = out_lb;
 }
 
+// Per-row arithmetic of the online pass, as a policy of fwd_pass.
+// SoftmaxRows keeps the five running scalars of Algorithm 1; SigmoidRows
+// keeps the sums of the sigmoid-score divergence. Each provides: State
+// (what a lane carries across tiles), Partial (what it stores, merges and
+// returns), init, update (one tile), partial, merge, and the NTOT floats per
+// thread that a chunk total takes in LDS.
+struct SoftmaxRows {
+  static constexpr int NTOT = 5;
+  struct State {
+    RowState st;
+    TileCarry tc;
+  };
+  typedef RowPartial Partial;
+  __device__ __forceinline__ static State init() { return State{RowState{kNegInf, 0.f, kNegInf, 0.f, 0.f}, {}}; }
+  __device__ __forceinline__ static void reset(State& s) { s.st = RowState{kNegInf, 0.f, kNegInf, 0.f, 0.f}; }
+  __device__ __forceinline__ static void update(State& s, const f32x16& sa, const f32x16& sb, float ca, float cb) {
+    fwd_update_first(s.st, s.tc, sa, sb, ca, cb);
+    fwd_update_second(s.st, s.tc, sa, sb, ca, cb);
+  }
+  __device__ __forceinline__ static Partial partial(const State& s, float ca, float cb) {
+    return state_partial(s.st, ca, cb);
+  }
+  __device__ __forceinline__ static Partial merge(const Partial& x, const Partial& y) { return merge_partials(x, y); }
+  __device__ __forceinline__ static void store(float* tot, int i, int n, const Partial& r) {
+    tot[i] = r.ma;
+    tot[n + i] = r.la;
+    tot[2 * n + i] = r.mb;
+    tot[3 * n + i] = r.lb;
+    tot[4 * n + i] = r.acc;
+  }
+  __device__ __forceinline__ static Partial load(const float* tot, int i, int n) {
+    return Partial{tot[i], tot[n + i], tot[2 * n + i], tot[3 * n + i], tot[4 * n + i]};
+  }
+  __device__ __forceinline__ static Partial halfwave(const Partial& p) { return halfwave_merge(p); }
+};
+
+// Sigmoid scores (Sec. 3.1, "Generalizability beyond Softmax"): A_t =
+// sigmoid(S_t) with no normalisation, and the row value is the generalized
+// KL sum_j [A_a log(A_a / A_b) - A_a + A_b] over the visible keys. With
+// nl = -log2 A (sigmoid_terms) a lane keeps four plain sums over its keys:
+// acc = sum A_a (nl_b - nl_a) (base 2), dif = sum (A_b - A_a) and the masses
+// sum A_a, sum A_b; L = acc ln 2 + dif. No maximum or rescaling is needed:
+// every term is bounded (A <= 1, |nl| <= |z| + 1). Chunk totals and the two
+// half-waves combine by addition.
+struct SigmoidPartial {
+  float acc, dif, ma, mb;
+};
+
+struct SigmoidRows {
+  static constexpr int NTOT = 4;
+  typedef SigmoidPartial State;
+  typedef SigmoidPartial Partial;
+  __device__ __forceinline__ static State init() { return State{0.f, 0.f, 0.f, 0.f}; }
+  __device__ __forceinline__ static void reset(State& s) { s = init(); }
+  __device__ __forceinline__ static void update(State& s, const f32x16& sa, const f32x16& sb, float ca, float cb) {
+    float acc[2] = {0.f, 0.f}, dif[2] = {0.f, 0.f}, ma[2] = {0.f, 0.f}, mb[2] = {0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const SigmoidTerms ta = sigmoid_terms(sa[i] * ca), tb = sigmoid_terms(sb[i] * cb);
+      const int k = i & 1;
+      acc[k] = __builtin_fmaf(ta.a, tb.nl - ta.nl, acc[k]);
+      dif[k] += tb.a - ta.a;
+      ma[k] += ta.a;
+      mb[k] += tb.a;
+    }
+    s.acc += acc[0] + acc[1];
+    s.dif += dif[0] + dif[1];
+    s.ma += ma[0] + ma[1];
+    s.mb += mb[0] + mb[1];
+  }
+  __device__ __forceinline__ static Partial partial(const State& s, float, float) { return s; }
+  __device__ __forceinline__ static Partial merge(const Partial& x, const Partial& y) {
+    return Partial{x.acc + y.acc, x.dif + y.dif, x.ma + y.ma, x.mb + y.mb};
+  }
+  __device__ __forceinline__ static void store(float* tot, int i, int n, const Partial& r) {
+    tot[i] = r.acc;
+    tot[n + i] = r.dif;
+    tot[2 * n + i] = r.ma;
+    tot[3 * n + i] = r.mb;
+  }
+  __device__ __forceinline__ static Partial load(const float* tot, int i, int n) {
+    return Partial{tot[i], tot[n + i], tot[2 * n + i], tot[3 * n + i]};
+  }
+  __device__ __forceinline__ static Partial halfwave(const Partial& p) {
+    return merge(p, Partial{__shfl_xor(p.acc, 32), __shfl_xor(p.dif, 32), __shfl_xor(p.ma, 32), __shfl_xor(p.mb, 32)});
+  }
+};
+
+// L and the masses of a complete sigmoid row; the masses are written where
+// the caller asked for them.
+__device__ __forceinline__ void write_row_sigmoid(const SigmoidPartial& p, size_t ri, float* __restrict__ kl,
+                                                  float* __restrict__ mass_a, float* __restrict__ mass_b) {
+  kl[ri] = __builtin_fmaf(p.acc, kLn2, p.dif);
+  if (mass_a) mass_a[ri] = p.ma;
+  if (mass_b) mass_b[ri] = p.mb;
+}
+
 // Row geometry shared by both kernels. Tiles 0 .. tlast hold keys some row of
 // the wave may see (-1: none); tiles from tmask on cross the causal diagonal
 // of some row of the wave or the ragged key tail.
@@ -315,8 +412,9 @@ struct FwdTraits {
 // rows q0 .. q0 + BQ - 1 of head bh; returns the lane's row state (both
 // half-waves merged) and its row index in myq. tot: LDS for the per-lane
 // totals of the chunked sums, 5 * NT floats.
-template <class C, bool CAUSAL>
-__device__ __forceinline__ RowPartial fwd_pass(u32x4* st0, u32x4* st1, float* tot, const uint16_t* __restrict__ Qa,
+template <class C, bool CAUSAL, class Rows = SoftmaxRows>
+__device__ __forceinline__ typename Rows::Partial fwd_pass(u32x4* st0, u32x4* st1, float* tot,
+                                                           const uint16_t* __restrict__ Qa,
                                                const uint16_t* __restrict__ Ka, const uint16_t* __restrict__ Qb,
                                                const uint16_t* __restrict__ Kb, int NQ, int NK, float ca, float cb,
                                                int bh, int q0, int t_begin, int t_end, int& myq) {
@@ -351,12 +449,8 @@ __device__ __forceinline__ RowPartial fwd_pass(u32x4* st0, u32x4* st1, float* to
   // operand bases of the row-padded layout (unused otherwise)
   const int base_a = C::PAD ? PadRows<C::CA>::base(lane & 31, half) : 0;
   const int base_b = C::PAD ? PadRows<C::CB>::base(lane & 31, half) : 0;
-  RowState st{kNegInf, 0.f, kNegInf, 0.f, 0.f};
-  TileCarry tc{};
+  typename Rows::State st = Rows::init();
   bool have_total = false;   // uniform: whether tot holds a chunk yet
-  auto load_total = [&]() {
-    return RowPartial{tot[tid], tot[C::NT + tid], tot[2 * C::NT + tid], tot[3 * C::NT + tid], tot[4 * C::NT + tid]};
-  };
 
   if (t_begin < t_end && streamer) {
     dma.issue(rka, rkb, t_begin * BK, st0, wave);
@@ -373,19 +467,14 @@ __device__ __forceinline__ RowPartial fwd_pass(u32x4* st0, u32x4* st1, float* to
       f32x16 sa, sb;
       fwd_logits<DA, DB, C::PAD>(cur, qa, qb, sa, sb, lane, base_a, base_b);
       if (t >= wt.tmask) mask_tile(sa, sb, t * BK + 4 * half, NK, kcm);
-      fwd_update_first(st, tc, sa, sb, ca, cb);
-      fwd_update_second(st, tc, sa, sb, ca, cb);
+      Rows::update(st, sa, sb, ca, cb);
     }
     if ((t - t_begin) % kFoldTiles == kFoldTiles - 1 && t + 1 < t_end) {
-      RowPartial r = state_partial(st, ca, cb);
-      if (have_total) r = merge_partials(load_total(), r);
-      tot[tid] = r.ma;
-      tot[C::NT + tid] = r.la;
-      tot[2 * C::NT + tid] = r.mb;
-      tot[3 * C::NT + tid] = r.lb;
-      tot[4 * C::NT + tid] = r.acc;
+      typename Rows::Partial r = Rows::partial(st, ca, cb);
+      if (have_total) r = Rows::merge(Rows::load(tot, tid, C::NT), r);
+      Rows::store(tot, tid, C::NT, r);
       have_total = true;
-      st = RowState{kNegInf, 0.f, kNegInf, 0.f, 0.f};
+      Rows::reset(st);
     }
     wait_vmem();          // tile t + 1 has landed (for this wave) ...
     barrier_no_fence();   // ... and for every wave
@@ -395,9 +484,9 @@ __device__ __forceinline__ RowPartial fwd_pass(u32x4* st0, u32x4* st1, float* to
     if (t + 1 < t_end) step(st1, st0, t + 1);
   }
   wait_vmem();   // no load may still target LDS when the workgroup ends
-  RowPartial mine = state_partial(st, ca, cb);
-  if (have_total) mine = merge_partials(load_total(), mine);
-  return halfwave_merge(mine);
+  typename Rows::Partial mine = Rows::partial(st, ca, cb);
+  if (have_total) mine = Rows::merge(Rows::load(tot, tid, C::NT), mine);
+  return Rows::halfwave(mine);
 }
 
 // Whole key range per workgroup: grid B*H * ceil(N_Q / BQ).
@@ -409,7 +498,7 @@ kl_fwd_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
               float* __restrict__ kl, float* __restrict__ lse_a, float* __restrict__ lse_b) {
   __shared__ u32x4 st0[C::STAGE];
   __shared__ u32x4 st1[C::STAGE];
-  __shared__ float tot[5 * C::NT];
+  __shared__ float tot[SoftmaxRows::NTOT * C::NT];
   const int TQ = (NQ + C::BQ - 1) / C::BQ;
   const int logical = xcd_logical(blockIdx.x, gridDim.x);
   const int bh = logical / TQ;
@@ -419,6 +508,28 @@ kl_fwd_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
   const RowPartial p =
       fwd_pass<C, CAUSAL>(st0, st1, tot, Qa, Ka, Qb, Kb, NQ, NK, ca, cb, bh, qt * C::BQ, 0, 1 << 30, myq);
   if ((threadIdx.x & 32) == 0 && myq < NQ) write_row(p, (size_t)bh * NQ + myq, kl, lse_a, lse_b);
+}
+
+// Forward of the sigmoid-score divergence (see SigmoidRows): the same tile
+// loop over the whole key range, grid B*H * ceil(N_Q / BQ).
+template <class C, bool CAUSAL>
+__global__ void __launch_bounds__(C::NT, C::WAVES_PER_SIMD)
+kl_fwd_sigmoid_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
+                      const uint16_t* __restrict__ Qb, const uint16_t* __restrict__ Kb,
+                      int NQ, int NK, float ca, float cb,
+                      float* __restrict__ kl, float* __restrict__ mass_a, float* __restrict__ mass_b) {
+  __shared__ u32x4 st0[C::STAGE];
+  __shared__ u32x4 st1[C::STAGE];
+  __shared__ float tot[SigmoidRows::NTOT * C::NT];
+  const int TQ = (NQ + C::BQ - 1) / C::BQ;
+  const int logical = xcd_logical(blockIdx.x, gridDim.x);
+  const int bh = logical / TQ;
+  int qt = logical - bh * TQ;
+  if (CAUSAL) qt = TQ - 1 - qt;   // longest rows first
+  int myq;
+  const SigmoidPartial p = fwd_pass<C, CAUSAL, SigmoidRows>(st0, st1, tot, Qa, Ka, Qb, Kb, NQ, NK, ca, cb, bh,
+                                                            qt * C::BQ, 0, 1 << 30, myq);
+  if ((threadIdx.x & 32) == 0 && myq < NQ) write_row_sigmoid(p, (size_t)bh * NQ + myq, kl, mass_a, mass_b);
 }
 
 // Split-K partial pass (Sec. 3.3): grid B*H * ceil(N_Q / BQ) * W; workgroup
@@ -432,7 +543,7 @@ kl_fwd_partial_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restric
                       int NQ, int NK, float ca, float cb, int W, int chunk, float* __restrict__ part) {
   __shared__ u32x4 st0[C::STAGE];
   __shared__ u32x4 st1[C::STAGE];
-  __shared__ float tot[5 * C::NT];
+  __shared__ float tot[SoftmaxRows::NTOT * C::NT];
   const int TQ = (NQ + C::BQ - 1) / C::BQ;
   const int logical = xcd_logical(blockIdx.x, gridDim.x);
   const int w = logical % W;
@@ -460,7 +571,7 @@ kl_fwd_partial_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restric
 // KL, LSE_a, LSE_b. One thread per row walking its W partials in sequence
 // spent a load latency per partial: 14-20 us at W = 32.
 constexpr int kMergeRowsPerBlock = 4;
-__global__ void __launch_bounds__(64 * kMergeRowsPerBlock)
+static __global__ void __launch_bounds__(64 * kMergeRowsPerBlock)
 kl_fwd_merge_kernel(const float* __restrict__ part, int W, size_t rows, float* __restrict__ kl,
                     float* __restrict__ lse_a, float* __restrict__ lse_b) {
   const int lane = threadIdx.x & 63;
@@ -504,5 +615,24 @@ using FwdCausalSmallCfg = FwdTraits<DA, DB, 2, 2, 4, true>;
 // one-wave or two four-wave workgroups per CU (one for wide heads).
 template <int DA, int DB, int NW>
 using FwdSmallCfg = FwdTraits<DA, DB, 2, (DA + DB <= 256) ? (NW == 1 ? 4 : 2) : 1, NW>;
+
+// Which configuration a head shape takes (the launch units instantiate
+// them): one wave for at most 32 query rows, four waves for at most 128
+// (d1 + d2 <= 256), the 128-row causal configuration when 256-row workgroups
+// would number fewer than four per CU, otherwise FwdCfg. The causal 128-row
+// configuration measured 10-16% faster on such shapes (twice the workgroups:
+// the two waves sharing a SIMD come from different workgroups and the long
+// causal rows spread over more CUs); non-causal shapes of the same size were
+// 4-6% slower with it and keep the default.
+enum class FwdShape { kOneWave, kFourWaves, kCausalSmall, kDefault };
+constexpr long long kCausalSmallGrid = 1024;
+inline FwdShape fwd_shape(int da, int db, int n_q, long long bh, bool causal) {
+  if (n_q <= 32) return FwdShape::kOneWave;
+  if (da + db <= 256) {
+    if (n_q <= 128) return FwdShape::kFourWaves;
+    if (causal && bh * ((n_q + 255) / 256) < kCausalSmallGrid) return FwdShape::kCausalSmall;
+  }
+  return FwdShape::kDefault;
+}
 
 }  // namespace streamkl

@@ -29,21 +29,17 @@ static hipError_t run_cfg(const FwdArgs& a, int W, float* part) {
   return hipGetLastError();
 }
 
-// Causal heads whose 256-row workgroups would number fewer than four per CU
-// run 128-row ones instead (FwdCausalSmallCfg): twice the workgroups, so the
-// two waves sharing a SIMD come from different workgroups (their phases are
-// not tied by one barrier) and the rows that see the most keys are spread
-// over more CUs. Measured 10-16% faster on such shapes; non-causal shapes of
-// the same size measured 4-6% slower, so they keep the default.
-constexpr long long kCausalSmallGrid = 1024;
-static bool causal_small_grid(long long bh, int n_q) { return bh * ((n_q + 255) / 256) < kCausalSmallGrid; }
-
 template <int DA, int DB, bool CAUSAL>
 static hipError_t run_fwd(const FwdArgs& a, int W, float* part) {
-  if (a.NQ <= 32) return run_cfg<DA, DB, CAUSAL, FwdSmallCfg<DA, DB, 1>>(a, W, part);
-  if constexpr (DA + DB <= 256) {
-    if (a.NQ <= 128) return run_cfg<DA, DB, CAUSAL, FwdSmallCfg<DA, DB, 4>>(a, W, part);
-    if (CAUSAL && causal_small_grid(a.BH, a.NQ)) return run_cfg<DA, DB, CAUSAL, FwdCausalSmallCfg<DA, DB>>(a, W, part);
+  switch (fwd_shape(DA, DB, a.NQ, a.BH, CAUSAL)) {
+    case FwdShape::kOneWave: return run_cfg<DA, DB, CAUSAL, FwdSmallCfg<DA, DB, 1>>(a, W, part);
+    case FwdShape::kFourWaves:
+      if constexpr (DA + DB <= 256) return run_cfg<DA, DB, CAUSAL, FwdSmallCfg<DA, DB, 4>>(a, W, part);
+      break;
+    case FwdShape::kCausalSmall:
+      if constexpr (DA + DB <= 256) return run_cfg<DA, DB, CAUSAL, FwdCausalSmallCfg<DA, DB>>(a, W, part);
+      break;
+    case FwdShape::kDefault: break;
   }
   return run_cfg<DA, DB, CAUSAL, FwdCfg<DA, DB>>(a, W, part);
 }
@@ -51,9 +47,13 @@ static hipError_t run_fwd(const FwdArgs& a, int W, float* part) {
 int fwd_merge_rows_per_workgroup() { return kMergeRowsPerBlock; }
 
 int fwd_rows_per_workgroup(int da, int db, int n_q, long long bh, bool causal) {
-  if (n_q <= 32) return 32;
-  if (da + db <= 256) return (n_q <= 128 || (causal && causal_small_grid(bh, n_q))) ? 128 : 256;
-  return 128;
+  switch (fwd_shape(da, db, n_q, bh, causal)) {
+    case FwdShape::kOneWave: return 32;
+    case FwdShape::kFourWaves:
+    case FwdShape::kCausalSmall: return 128;
+    case FwdShape::kDefault: break;
+  }
+  return da + db <= 256 ? 256 : 128;
 }
 
 hipError_t launch_fwd(int da, int db, bool causal, const FwdArgs& a, int W, float* part) {

@@ -23,6 +23,7 @@ struct BwdArgs {
   float sa, sb;
   const float *kl, *lse_a, *lse_b, *g;
   float *dQa, *dQb, *dKa, *dKb;
+  int act;                      // 0: softmax scores; 1: sigmoid scores (kl and the LSEs unused)
   hipStream_t stream;
 };
 
@@ -31,6 +32,9 @@ struct BwdArgs {
 // W <= 1: one pass over all keys. W > 1: split-K (Sec. 3.3) with W key chunks;
 // part holds 5 * W * BH * NQ floats of partial row statistics.
 hipError_t launch_fwd(int da, int db, bool causal, const FwdArgs& a, int W, float* part);
+// Sigmoid-score forward (one pass): kl, and the row masses of the first and
+// second slot in lse_a / lse_b (either may be null). ca, cb are s * log2(e).
+hipError_t launch_fwd_sigmoid(int da, int db, bool causal, const FwdArgs& a);
 // Query rows per workgroup of the forward for these head dims, rows per head,
 // number of heads and mask.
 int fwd_rows_per_workgroup(int da, int db, int n_q, long long bh, bool causal);
@@ -44,6 +48,12 @@ hipError_t launch_bwd_dq_m3(int da, int db, bool causal, const BwdArgs& a);
 hipError_t launch_bwd_dk_m1(int da, int db, bool causal, const BwdArgs& a);
 hipError_t launch_bwd_dk_m2(int da, int db, bool causal, const BwdArgs& a);
 hipError_t launch_bwd_dk_m3(int da, int db, bool causal, const BwdArgs& a);
+hipError_t launch_bwd_dq_sig_m1(int da, int db, bool causal, const BwdArgs& a);
+hipError_t launch_bwd_dq_sig_m2(int da, int db, bool causal, const BwdArgs& a);
+hipError_t launch_bwd_dq_sig_m3(int da, int db, bool causal, const BwdArgs& a);
+hipError_t launch_bwd_dk_sig_m1(int da, int db, bool causal, const BwdArgs& a);
+hipError_t launch_bwd_dk_sig_m2(int da, int db, bool causal, const BwdArgs& a);
+hipError_t launch_bwd_dk_sig_m3(int da, int db, bool causal, const BwdArgs& a);
 // Fused backward (Sec. 4.2): one key-owned kernel writes dK and adds dQ with
 // atomics; dQ must be zeroed first. bwd_fused_fits says whether the kernel
 // exists for these head dims and mode (its working set must fit in LDS).

@@ -158,6 +158,36 @@ extern "C" int streamkl_fwd(const void* Q1, const void* K1, const void* Q2, cons
                     lse1, lse2, stream);
 }
 
+extern "C" int streamkl_fwd_act(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H,
+                                int N_Q, int N_K, int d1, int d2, float s1, float s2, int causal, int direction,
+                                int activation, float* kl, float* stat1, float* stat2, hipStream_t stream) {
+  if (activation == STREAMKL_ACT_SOFTMAX)
+    return fwd_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, 1, nullptr, 0, false, kl,
+                      stat1, stat2, stream);
+  if (activation != STREAMKL_ACT_SIGMOID) return STREAMKL_ERR_INVALID_ARG;
+  bool empty = false;
+  const int st = check_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, &empty);
+  if (st != STREAMKL_OK || empty) return st;
+  if (!kl || !aligned(kl, 4) || (stat1 && !aligned(stat1, 4)) || (stat2 && !aligned(stat2, 4)))
+    return STREAMKL_ERR_INVALID_ARG;
+  const bool rev = direction == STREAMKL_KL_REV;
+  FwdArgs a;
+  a.Qa = static_cast<const uint16_t*>(rev ? Q2 : Q1);
+  a.Ka = static_cast<const uint16_t*>(rev ? K2 : K1);
+  a.Qb = static_cast<const uint16_t*>(rev ? Q1 : Q2);
+  a.Kb = static_cast<const uint16_t*>(rev ? K1 : K2);
+  a.BH = B * H;
+  a.NQ = N_Q;
+  a.NK = N_K;
+  a.ca = (rev ? s2 : s1) * kLog2e;
+  a.cb = (rev ? s1 : s2) * kLog2e;
+  a.kl = kl;
+  a.lse_a = rev ? stat2 : stat1;
+  a.lse_b = rev ? stat1 : stat2;
+  a.stream = stream;
+  return hip_status(streamkl::launch_fwd_sigmoid(rev ? d2 : d1, rev ? d1 : d2, causal == 1, a));
+}
+
 extern "C" int streamkl_fwd_split(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H,
                                   int N_Q, int N_K, int d1, int d2, float s1, float s2, int causal, int direction,
                                   int splits, void* workspace, size_t workspace_bytes, float* kl, float* lse1,
@@ -217,10 +247,12 @@ bool fused_preferred(int N_Q, int N_K) {
   return tq * kFusedRatio <= tk && tq <= kFusedMaxQueryTiles;
 }
 
+// act: STREAMKL_ACT_SOFTMAX or STREAMKL_ACT_SIGMOID (kl, lse1, lse2 unused
+// and not required; separate kernels only).
 int bwd_common(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H, int N_Q, int N_K,
                int d1, int d2, float s1, float s2, int causal, int direction, const float* kl, const float* lse1,
                const float* lse2, const float* dkl, float* dQ1, float* dK1, float* dQ2, float* dK2, int strategy,
-               hipStream_t stream) {
+               int act, hipStream_t stream) {
   if (!dQ1 && !dK1 && !dQ2 && !dK2) return STREAMKL_ERR_INVALID_ARG;
   if (strategy != STREAMKL_BWD_AUTO && strategy != STREAMKL_BWD_SEPARATE && strategy != STREAMKL_BWD_FUSED)
     return STREAMKL_ERR_INVALID_ARG;
@@ -230,7 +262,8 @@ int bwd_common(const void* Q1, const void* K1, const void* Q2, const void* K2, i
   const bool rev = direction == STREAMKL_KL_REV;
   const int da = rev ? d2 : d1, db = rev ? d1 : d2;
   const BwdModes m = bwd_modes(rev, dQ1, dK1, dQ2, dK2);
-  const bool fused_ok = m.q != 0 && streamkl::bwd_fused_fits(da, db, m.q | m.k);
+  const bool sig = act == STREAMKL_ACT_SIGMOID;
+  const bool fused_ok = !sig && m.q != 0 && streamkl::bwd_fused_fits(da, db, m.q | m.k);
   if (strategy == STREAMKL_BWD_FUSED && m.q != 0 && !fused_ok) return STREAMKL_ERR_UNSUPPORTED;
   const bool fused = fused_ok && (strategy == STREAMKL_BWD_FUSED ||
                                   (strategy == STREAMKL_BWD_AUTO && fused_preferred(N_Q, N_K)));
@@ -244,7 +277,7 @@ int bwd_common(const void* Q1, const void* K1, const void* Q2, const void* K2, i
     if (e == hipSuccess) e = zero_fill(dK2, (size_t)bh * N_K * d2, stream);
     return hip_status(e);
   }
-  if (!kl || !lse1 || !lse2) return STREAMKL_ERR_INVALID_ARG;
+  if (!sig && (!kl || !lse1 || !lse2)) return STREAMKL_ERR_INVALID_ARG;
   const void* ptrs[] = {kl, lse1, lse2, dkl, dQ1, dK1, dQ2, dK2};
   for (const void* p : ptrs)
     if (p && !aligned(p, 4)) return STREAMKL_ERR_INVALID_ARG;
@@ -266,6 +299,7 @@ int bwd_common(const void* Q1, const void* K1, const void* Q2, const void* K2, i
   a.dQb = rev ? dQ1 : dQ2;
   a.dKa = rev ? dK2 : dK1;
   a.dKb = rev ? dK1 : dK2;
+  a.act = sig ? 1 : 0;
   a.stream = stream;
   hipError_t e = hipSuccess;
   if (m.q && N_K == 0) {   // every row is empty: zero gradients
@@ -292,7 +326,7 @@ extern "C" int streamkl_bwd(const void* Q1, const void* K1, const void* Q2, cons
                             const float* kl, const float* lse1, const float* lse2, const float* dkl, float* dQ1,
                             float* dK1, float* dQ2, float* dK2, hipStream_t stream) {
   return bwd_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, kl, lse1, lse2, dkl, dQ1,
-                    dK1, dQ2, dK2, STREAMKL_BWD_SEPARATE, stream);
+                    dK1, dQ2, dK2, STREAMKL_BWD_SEPARATE, STREAMKL_ACT_SOFTMAX, stream);
 }
 
 extern "C" int streamkl_bwd_ex(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H,
@@ -300,7 +334,16 @@ extern "C" int streamkl_bwd_ex(const void* Q1, const void* K1, const void* Q2, c
                                const float* kl, const float* lse1, const float* lse2, const float* dkl,
                                float* dQ1, float* dK1, float* dQ2, float* dK2, int strategy, hipStream_t stream) {
   return bwd_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, kl, lse1, lse2, dkl, dQ1,
-                    dK1, dQ2, dK2, strategy, stream);
+                    dK1, dQ2, dK2, strategy, STREAMKL_ACT_SOFTMAX, stream);
+}
+
+extern "C" int streamkl_bwd_act(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H,
+                                int N_Q, int N_K, int d1, int d2, float s1, float s2, int causal, int direction,
+                                int activation, const float* kl, const float* stat1, const float* stat2,
+                                const float* dkl, float* dQ1, float* dK1, float* dQ2, float* dK2, hipStream_t stream) {
+  if (activation != STREAMKL_ACT_SOFTMAX && activation != STREAMKL_ACT_SIGMOID) return STREAMKL_ERR_INVALID_ARG;
+  return bwd_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, kl, stat1, stat2, dkl, dQ1,
+                    dK1, dQ2, dK2, STREAMKL_BWD_SEPARATE, activation, stream);
 }
 
 extern "C" int streamkl_bwd_choose(int B, int H, int N_Q, int N_K, int d1, int d2, int causal, int direction,
@@ -335,6 +378,14 @@ extern "C" int streamkl_supported_head_dim(int d) { return supported_dim(d) ? 1 
 namespace streamkl {
 
 hipError_t launch_bwd_dq(int da, int db, bool causal, int mode, const BwdArgs& a) {
+  if (a.act == 1) {
+    switch (mode) {
+      case 1: return launch_bwd_dq_sig_m1(da, db, causal, a);
+      case 2: return launch_bwd_dq_sig_m2(da, db, causal, a);
+      case 3: return launch_bwd_dq_sig_m3(da, db, causal, a);
+      default: return hipErrorInvalidValue;
+    }
+  }
   switch (mode) {
     case 1: return launch_bwd_dq_m1(da, db, causal, a);
     case 2: return launch_bwd_dq_m2(da, db, causal, a);
@@ -362,6 +413,14 @@ hipError_t launch_bwd_fused(int da, int db, bool causal, int mode, const BwdArgs
 }
 
 hipError_t launch_bwd_dk(int da, int db, bool causal, int mode, const BwdArgs& a) {
+  if (a.act == 1) {
+    switch (mode) {
+      case 1: return launch_bwd_dk_sig_m1(da, db, causal, a);
+      case 2: return launch_bwd_dk_sig_m2(da, db, causal, a);
+      case 3: return launch_bwd_dk_sig_m3(da, db, causal, a);
+      default: return hipErrorInvalidValue;
+    }
+  }
   switch (mode) {
     case 1: return launch_bwd_dk_m1(da, db, causal, a);
     case 2: return launch_bwd_dk_m2(da, db, causal, a);

@@ -25,9 +25,11 @@ NOALLOC_SCRATCH_BYTES = 16 << 20
 FWD, REV = 0, 1
 BWD_AUTO, BWD_SEPARATE, BWD_FUSED = 0, 1, 2
 GRAD_BITS = {"dq1": 1, "dk1": 2, "dq2": 4, "dk2": 8}
+ACT_SOFTMAX, ACT_SIGMOID = 0, 1
 ENTRY_POINTS = ("streamkl_fwd", "streamkl_bwd", "streamkl_bwd_ex", "streamkl_bwd_choose", "streamkl_fwd_split",
                 "streamkl_fwd_split_noalloc", "streamkl_fwd_split_workspace_bytes", "streamkl_fwd_split_count",
-                "streamkl_strerror", "streamkl_version", "streamkl_supported_head_dim")
+                "streamkl_fwd_act", "streamkl_bwd_act", "streamkl_strerror", "streamkl_version",
+                "streamkl_supported_head_dim")
 
 
 def _load():
@@ -43,6 +45,11 @@ def _load():
     lib.streamkl_bwd_ex.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, f, f, i, i, vp, vp, vp, vp, vp, vp, vp, vp, i,
                                     vp]
     lib.streamkl_bwd_ex.restype = i
+    lib.streamkl_fwd_act.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, f, f, i, i, i, vp, vp, vp, vp]
+    lib.streamkl_fwd_act.restype = i
+    lib.streamkl_bwd_act.argtypes = [vp, vp, vp, vp, i, i, i, i, i, i, f, f, i, i, i, vp, vp, vp, vp, vp, vp, vp,
+                                     vp, vp]
+    lib.streamkl_bwd_act.restype = i
     lib.streamkl_bwd_choose.argtypes = [i, i, i, i, i, i, i, i, i]
     lib.streamkl_bwd_choose.restype = i
     sz = ctypes.c_size_t
@@ -146,6 +153,36 @@ def fwd(q1, k1, q2, k2, s1=None, s2=None, causal=False, direction=FWD, out=None)
     return kl, lse1, lse2
 
 
+def _activation(activation) -> int:
+    if activation in (ACT_SOFTMAX, "softmax"):
+        return ACT_SOFTMAX
+    if activation in (ACT_SIGMOID, "sigmoid"):
+        return ACT_SIGMOID
+    raise ValueError(f"activation must be 'softmax' or 'sigmoid', got {activation!r}")
+
+
+def fwd_act(q1, k1, q2, k2, s1=None, s2=None, causal=False, direction=FWD, activation="sigmoid", out=None):
+    """streamkl_fwd_act: returns (kl, stat1, stat2), float32 [B, H, N_Q].
+
+    activation "softmax": exactly fwd (the stats are the LSEs). "sigmoid":
+    unnormalised sigmoid scores, kl is the generalized KL of the two score
+    rows and the stats are the row masses sum_j sigmoid(S_t[j]).
+    """
+    B, H, NQ, NK, d1, d2 = _check_inputs(q1, k1, q2, k2)
+    s1, s2 = _scales(s1, s2, d1, d2)
+    dev = q1.device
+    if out is None:
+        out = tuple(torch.empty((B, H, NQ), dtype=torch.float32, device=dev) for _ in range(3))
+    kl, st1, st2 = (_f32_rows(t, (B, H, NQ), dev, n) for t, n in zip(out, ("kl", "stat1", "stat2")))
+    with torch.cuda.device(dev):
+        st = lib.streamkl_fwd_act(_p(q1), _p(k1), _p(q2), _p(k2), B, H, NQ, NK, d1, d2, s1, s2, int(bool(causal)),
+                                  _direction(direction), _activation(activation), _p(kl), _p(st1), _p(st2),
+                                  _stream(dev))
+    if st != OK:
+        raise StreamKLError(st, "streamkl_fwd_act")
+    return kl, st1, st2
+
+
 def split_count(B, H, n_q, n_k, d1, d2) -> int:
     """streamkl_fwd_split_count: the adaptive split count of Sec. 3.3 (0 for invalid arguments)."""
     return int(lib.streamkl_fwd_split_count(int(B), int(H), int(n_q), int(n_k), int(d1), int(d2)))
@@ -228,14 +265,18 @@ def bwd_choose(B, H, n_q, n_k, d1, d2, causal=False, direction=FWD, want=("dq2",
 
 
 def bwd(q1, k1, q2, k2, kl, lse1, lse2, dkl=None, s1=None, s2=None, causal=False, direction=FWD,
-        want=("dq2", "dk2"), out=None, strategy="separate"):
-    """streamkl_bwd / streamkl_bwd_ex: returns (dQ1, dK1, dQ2, dK2), float32, None where not requested.
+        want=("dq2", "dk2"), out=None, strategy="separate", activation="softmax"):
+    """streamkl_bwd / streamkl_bwd_ex / streamkl_bwd_act: returns (dQ1, dK1, dQ2, dK2), float32, None where not
+    requested.
 
     want: any of "dq1", "dk1", "dq2", "dk2". dkl: per-row upstream gradient
     (float32 [B, H, N_Q]) or None for all ones. ``out`` may map those names to
     preallocated tensors. strategy: "separate" (streamkl_bwd, reproducible),
     "fused" (one kernel, dQ by atomics) or "auto" (the adaptive rule).
+    activation "sigmoid" (streamkl_bwd_act, separate kernels): kl, lse1, lse2
+    are not needed and may be None.
     """
+    act = _activation(activation)
     B, H, NQ, NK, d1, d2 = _check_inputs(q1, k1, q2, k2)
     s1, s2 = _scales(s1, s2, d1, d2)
     dev = q1.device
@@ -260,7 +301,11 @@ def bwd(q1, k1, q2, k2, kl, lse1, lse2, dkl=None, s1=None, s2=None, causal=False
             _p(kl), _p(lse1), _p(lse2), _p(dkl), _p(grads["dq1"]), _p(grads["dk1"]), _p(grads["dq2"]),
             _p(grads["dk2"]))
     with torch.cuda.device(dev):
-        if strat == BWD_SEPARATE:
+        if act == ACT_SIGMOID:
+            if strat != BWD_SEPARATE:
+                raise ValueError("sigmoid scores run the separate backward kernels only")
+            st, where = lib.streamkl_bwd_act(*args[:14], act, *args[14:], _stream(dev)), "streamkl_bwd_act"
+        elif strat == BWD_SEPARATE:
             st, where = lib.streamkl_bwd(*args, _stream(dev)), "streamkl_bwd"
         else:
             st, where = lib.streamkl_bwd_ex(*args, strat, _stream(dev)), "streamkl_bwd_ex"
@@ -271,41 +316,47 @@ def bwd(q1, k1, q2, k2, kl, lse1, lse2, dkl=None, s1=None, s2=None, causal=False
 
 class _AttentionKL(torch.autograd.Function):
     @staticmethod
-    def forward(ctx, q1, k1, q2, k2, s1, s2, causal, direction, bwd_strategy):
-        # the adaptive split count is 1 (the single-pass kernel) unless the heads have few query rows
-        kl, lse1, lse2 = fwd_split(q1, k1, q2, k2, s1, s2, causal, direction, splits="auto")
-        ctx.save_for_backward(q1, k1, q2, k2, kl, lse1, lse2)
-        ctx.cfg = (s1, s2, causal, direction, bwd_strategy)
-        ctx.mark_non_differentiable(lse1, lse2)
-        return kl, lse1, lse2
+    def forward(ctx, q1, k1, q2, k2, s1, s2, causal, direction, bwd_strategy, act):
+        if act == ACT_SIGMOID:
+            kl, st1, st2 = fwd_act(q1, k1, q2, k2, s1, s2, causal, direction, ACT_SIGMOID)
+        else:
+            # the adaptive split count is 1 (the single-pass kernel) unless the heads have few query rows
+            kl, st1, st2 = fwd_split(q1, k1, q2, k2, s1, s2, causal, direction, splits="auto")
+        ctx.save_for_backward(q1, k1, q2, k2, kl, st1, st2)
+        ctx.cfg = (s1, s2, causal, direction, bwd_strategy, act)
+        ctx.mark_non_differentiable(st1, st2)
+        return kl, st1, st2
 
     @staticmethod
-    def backward(ctx, gkl, _glse1, _glse2):
-        q1, k1, q2, k2, kl, lse1, lse2 = ctx.saved_tensors
-        s1, s2, causal, direction, strategy = ctx.cfg
+    def backward(ctx, gkl, _g1, _g2):
+        q1, k1, q2, k2, kl, st1, st2 = ctx.saved_tensors
+        s1, s2, causal, direction, strategy, act = ctx.cfg
         names = [n for n, need in zip(("dq1", "dk1", "dq2", "dk2"), ctx.needs_input_grad[:4]) if need]
         if not names:
-            return (None,) * 9
+            return (None,) * 10
         g = gkl.to(torch.float32).contiguous()
-        dq1, dk1, dq2, dk2 = bwd(q1, k1, q2, k2, kl, lse1, lse2, g, s1, s2, causal, direction, want=names,
-                                 strategy=strategy)
+        dq1, dk1, dq2, dk2 = bwd(q1, k1, q2, k2, kl, st1, st2, g, s1, s2, causal, direction, want=names,
+                                 strategy="separate" if act == ACT_SIGMOID else strategy, activation=act)
         cast = lambda t, ref: None if t is None else t.to(ref.dtype)   # noqa: E731
-        return cast(dq1, q1), cast(dk1, k1), cast(dq2, q2), cast(dk2, k2), None, None, None, None, None
+        return cast(dq1, q1), cast(dk1, k1), cast(dq2, q2), cast(dk2, k2), None, None, None, None, None, None
 
 
 def attention_kl(q1, k1, q2, k2, *, s1=None, s2=None, causal=False, direction="fwd", return_lse=False,
-                 bwd_strategy="auto"):
+                 bwd_strategy="auto", activation="softmax"):
     """Per-row KL between softmax(s1 q1 k1^T) and softmax(s2 q2 k2^T), differentiable.
 
-    Returns kl [B, H, N_Q] (and lse1, lse2 if ``return_lse``). The paper's
-    training objective is ``attention_kl(...).mean()``. Gradients flow to the
-    inputs that require them: (q2, k2) in standard distillation (Setting 1),
+    Returns kl [B, H, N_Q] (and the two row statistics if ``return_lse``:
+    lse1, lse2 for softmax, the row masses for sigmoid). The paper's training
+    objective is ``attention_kl(...).mean()``. Gradients flow to the inputs
+    that require them: (q2, k2) in standard distillation (Setting 1),
     (q1, k1) when the first distribution is trained (Setting 2), or both.
     bwd_strategy: "auto" (the adaptive rule of streamkl_bwd_choose), "fused"
-    or "separate" (bitwise reproducible gradients).
+    or "separate" (bitwise reproducible gradients). activation "sigmoid":
+    unnormalised sigmoid scores and the generalized KL (streamkl_fwd_act).
     """
     d1, d2 = q1.shape[-1], q2.shape[-1]
     s1, s2 = _scales(s1, s2, d1, d2)
     _strategy(bwd_strategy)
-    kl, lse1, lse2 = _AttentionKL.apply(q1, k1, q2, k2, s1, s2, bool(causal), _direction(direction), bwd_strategy)
-    return (kl, lse1, lse2) if return_lse else kl
+    kl, st1, st2 = _AttentionKL.apply(q1, k1, q2, k2, s1, s2, bool(causal), _direction(direction), bwd_strategy,
+                                      _activation(activation))
+    return (kl, st1, st2) if return_lse else kl

@@ -240,3 +240,42 @@ def test_noalloc_scratch_limit_is_the_header_constant(sk):
     w_max = sk.NOALLOC_SCRATCH_BYTES // (20 * 1024)
     assert sk.split_workspace_bytes(16, 1, 64, w_max) <= sk.NOALLOC_SCRATCH_BYTES
     assert noalloc_call(sk, splits=w_max + 1) == sk.ERR_SCRATCH_LIMIT
+
+
+def act_fwd_call(sk, **kw):
+    a = dict(Q1=FAKE, K1=FAKE, Q2=FAKE, K2=FAKE, B=1, H=2, NQ=64, NK=64, d1=64, d2=64, s1=0.125, s2=0.125,
+             causal=0, direction=0, act=1, kl=FAKE, st1=None, st2=None, stream=None)
+    a.update(kw)
+    return sk.lib.streamkl_fwd_act(a["Q1"], a["K1"], a["Q2"], a["K2"], a["B"], a["H"], a["NQ"], a["NK"], a["d1"],
+                                   a["d2"], a["s1"], a["s2"], a["causal"], a["direction"], a["act"], a["kl"],
+                                   a["st1"], a["st2"], a["stream"])
+
+
+def act_bwd_call(sk, **kw):
+    a = dict(Q1=FAKE, K1=FAKE, Q2=FAKE, K2=FAKE, B=1, H=2, NQ=64, NK=64, d1=64, d2=64, s1=0.125, s2=0.125,
+             causal=0, direction=0, act=1, kl=None, st1=None, st2=None, dkl=None, dQ1=None, dK1=None, dQ2=FAKE,
+             dK2=FAKE, stream=None)
+    a.update(kw)
+    return sk.lib.streamkl_bwd_act(a["Q1"], a["K1"], a["Q2"], a["K2"], a["B"], a["H"], a["NQ"], a["NK"], a["d1"],
+                                   a["d2"], a["s1"], a["s2"], a["causal"], a["direction"], a["act"], a["kl"],
+                                   a["st1"], a["st2"], a["dkl"], a["dQ1"], a["dK1"], a["dQ2"], a["dK2"], a["stream"])
+
+
+@pytest.mark.parametrize("call", [act_fwd_call, act_bwd_call])
+@pytest.mark.parametrize("kw,expect", [
+    (dict(act=2), 1), (dict(act=-1), 1), (dict(Q1=None), 1), (dict(K2=None), 1), (dict(NQ=-1), 1),
+    (dict(s1=0.0), 1), (dict(causal=2), 1), (dict(Q2=MIS), 1), (dict(d1=96), 2), (dict(B=0), 0),
+])
+def test_activation_argument_checks(sk, call, kw, expect):
+    assert call(sk, **kw) == expect
+
+
+def test_activation_specific_checks(sk):
+    # sigmoid forward: kl required, the masses optional but aligned when given
+    assert act_fwd_call(sk, kl=None) == 1
+    assert act_fwd_call(sk, st1=ctypes.c_void_p(0x100002)) == 1
+    # softmax through the act entry points keeps streamkl_fwd / streamkl_bwd's requirements
+    assert act_fwd_call(sk, act=0, st1=None) == 1
+    assert act_bwd_call(sk, act=0) == 1          # kl, lse1, lse2 missing
+    # sigmoid backward: no saved statistic needed, one gradient needed
+    assert act_bwd_call(sk, dQ2=None, dK2=None) == 1
