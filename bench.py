@@ -39,10 +39,11 @@ Timing (the method of the measurement plan):
 Side sections (each can be switched off): the 64K causal long-context
 workload ("long_context"), the other causal workloads ("workloads"), the
 split-K forward and the backward strategies on decode-like shapes
-("split_k", "fused_bwd") and the clock probe ("clock_probe").
+("split_k", "fused_bwd"), the sigmoid-score path ("sigmoid") and the clock
+probe ("clock_probe").
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--reps R] [--no-64k] [--no-cpu-baseline]
-                    [--no-split] [--no-fused] [--no-workloads] [--no-clock-probe] [--no-mfma-peak]
+                    [--no-split] [--no-fused] [--no-workloads] [--no-clock-probe] [--no-mfma-peak] [--no-sigmoid]
 """
 from __future__ import annotations
 
@@ -390,6 +391,43 @@ def fused_bwd_figures(sk, evict, reps=10):
             "rows": out}
 
 
+def sigmoid_figures(sk, evict, reps=10):
+    """The sigmoid-score path (streamkl_fwd_act / streamkl_bwd_act, Sec. 3.1)
+    on the mid shape (32 heads, 16384 x 16384, d1 = d2 = 128, seeded N(0,1)
+    drawn on the device), non-causal and causal: forward, dQ2 and dK2 kernels,
+    median of `reps` event-timed calls each after a cache-evicting write.
+    TFLOP/s count the same MFMA work as the softmax path; the kernels
+    themselves are bound by vector and transcendental issue (three
+    transcendental instructions per score and distribution)."""
+    import torch
+    B, H, N, D = 1, 32, 16384, 128
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(2606200050 + 10)
+    q1, k1, q2, k2 = (torch.randn((B, H, N, D), generator=gen, device="cuda").to(torch.bfloat16) for _ in range(4))
+    s = D ** -0.5
+    g = torch.full((B, H, N), 1.0 / (B * H * N), device="cuda")
+    dq2, dk2 = torch.empty((B, H, N, D), device="cuda"), torch.empty((B, H, N, D), device="cuda")
+    out = []
+    f = flops_per_pair(D, D)
+    for causal in (False, True):
+        P = B * H * (N * (N + 1) // 2 if causal else N * N)
+        fns = {"fwd": lambda: sk.fwd_act(q1, k1, q2, k2, s, s, causal, 0, "sigmoid"),
+               "dq": lambda: sk.bwd(q1, k1, q2, k2, None, None, None, g, s, s, causal, 0, want=("dq2",),
+                                    out={"dq2": dq2}, activation="sigmoid"),
+               "dk": lambda: sk.bwd(q1, k1, q2, k2, None, None, None, g, s, s, causal, 0, want=("dk2",),
+                                    out={"dk2": dk2}, activation="sigmoid")}
+        row = {"causal": causal, "pairs": P}
+        for k, fn in fns.items():
+            med, _ = timed_reps(fn, reps, evict)
+            row[f"{k}_ms"] = round(med, 4)
+            row[f"{k}_tflops"] = round(f[k] * P / (med * 1e-3) / 1e12, 2)
+        row["bwd_tflops_algorithmic"] = round(f["bwd"] * P / ((row["dq_ms"] + row["dk_ms"]) * 1e-3) / 1e12, 2)
+        out.append(row)
+    del q1, k1, q2, k2, dq2, dk2
+    torch.cuda.empty_cache()
+    return {"workload": f"sigmoid scores, generalized KL: B={B} H={H} N_Q=N_K={N} d1=d2={D}", "rows": out}
+
+
 # ---------------------------------------------------------------------------- CPU baseline (the fp64 oracle)
 
 _CPU = {}
@@ -492,6 +530,7 @@ def main():
     ap.add_argument("--no-clock-probe", action="store_true",
                     help="skip timing the mid forward and a library GEMM on random and on constant operands")
     ap.add_argument("--no-mfma-peak", action="store_true", help="skip the measured MFMA peak")
+    ap.add_argument("--no-sigmoid", action="store_true", help="skip the sigmoid-score figures")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run one 1 GiB device copy (reference kernel for HBM counters)")
     a = ap.parse_args()
@@ -588,6 +627,8 @@ def main():
         res["split_k"] = split_k_figures(sk, evict)
     if not a.no_fused:
         res["fused_bwd"] = fused_bwd_figures(sk, evict)
+    if not a.no_sigmoid:
+        res["sigmoid"] = sigmoid_figures(sk, evict)
     if not a.no_clock_probe:
         res["clock_probe"] = clock_figures(sk)
     if a.copy_calibration:

@@ -33,7 +33,10 @@
  * - direction = STREAMKL_KL_FWD evaluates KL(P1 || P2) (the paper's
  *   objective); STREAMKL_KL_REV evaluates KL(P2 || P1). lse1/lse2 always
  *   belong to (Q1,K1,s1) / (Q2,K2,s2).
- * - Supported head dims: d1, d2 in {64, 128, 192, 256}.
+ * - Supported head dims: d1, d2 in {32, 64, 96, ..., 256} (multiples of 32).
+ *   The kernels are built for multiples of 64; 32, 96, 160 and 224 run those
+ *   of the next multiple of 64 with the missing columns read as zeros, so
+ *   their matrix work is that of the wider head.
  * - B, H, N_Q, N_K >= 0; a zero extent is a valid call that launches
  *   nothing (N_K = 0 with N_Q > 0 makes every row empty). One head's rows
  *   of any tensor must span less than 4 GiB as fp32 (N * max(d1, d2) * 4 <
@@ -58,7 +61,7 @@ extern "C" {
 typedef enum {
   STREAMKL_OK = 0,
   STREAMKL_ERR_INVALID_ARG = 1, /* NULL pointer, negative extent, bad flag, scale, alignment */
-  STREAMKL_ERR_UNSUPPORTED = 2, /* head dim outside {64, 128, 192, 256}, extent too large  */
+  STREAMKL_ERR_UNSUPPORTED = 2, /* head dim not in {32, 64, ..., 256}, extent too large     */
   STREAMKL_ERR_HIP = 3,         /* a kernel launch was rejected by the HIP runtime          */
   STREAMKL_ERR_SCRATCH_LIMIT = 4 /* streamkl_fwd_split_noalloc: partials exceed its scratch */
 } streamkl_status;
@@ -145,7 +148,8 @@ int streamkl_bwd(const void* Q1, const void* K1, const void* Q2, const void* K2,
  *                          and the fused kernel's working set does not fit
  *                          in LDS for these head dims (only when gradients
  *                          of both distributions are requested and
- *                          d1 + d2 > 320).
+ *                          d1 + d2 > 320), or when a head dim is not a
+ *                          multiple of 64.
  *   STREAMKL_BWD_AUTO      the strategy streamkl_bwd_choose returns.
  * With no dQ requested every strategy runs the dK kernel alone.
  */
@@ -161,7 +165,8 @@ int streamkl_bwd_ex(const void* Q1, const void* K1, const void* Q2, const void* 
  * Adaptive strategy selection (Sec. 4.2): with T_Q and T_K the numbers of
  * 128-row query and key tiles per head, returns STREAMKL_BWD_FUSED when
  * T_Q * C <= T_K (dQ small next to dK, so its atomics stay cheap) with C = 8,
- * T_Q <= 4, and the fused kernel exists for the request; else
+ * T_Q <= 4, and the fused kernel exists for the request (head dims that
+ * are multiples of 64, working set within LDS); else
  * STREAMKL_BWD_SEPARATE. The constants were measured on MI355X: there the
  * fused kernel loses beyond 512 query rows at any N_K. `grads` is an OR of
  * STREAMKL_GRAD_* bits. Returns 0 for invalid or unsupported arguments.

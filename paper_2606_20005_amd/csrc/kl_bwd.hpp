@@ -335,51 +335,63 @@ __device__ __forceinline__ void bwd_tile(const u32x4* stage, const bf16x8 (&ra_o
 }
 
 // Resident rows of this lane as MFMA B operands (zero rows past n).
+// dreal: the row length in global memory (D, or less for a padded head dim:
+// the chunks past it are zeros).
 template <int D>
 __device__ __forceinline__ void load_resident(bf16x8 (&op)[D / 16], const uint16_t* X, size_t bh_rows, int row,
-                                              int n, int half) {
+                                              int n, int half, int dreal = D) {
   const bool ok = row < n;
-  const u32x4* p = reinterpret_cast<const u32x4*>(X + (bh_rows + (ok ? row : 0)) * D);
+  const u32x4* p = reinterpret_cast<const u32x4*>(X + (bh_rows + (ok ? row : 0)) * dreal);
 #pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks)
-    op[ks] = __builtin_bit_cast(bf16x8, ok ? p[2 * ks + half] : u32x4{0u, 0u, 0u, 0u});
+  for (int ks = 0; ks < D / 16; ++ks) {
+    const int c = 2 * ks + half;
+    op[ks] = __builtin_bit_cast(bf16x8, ok && 8 * c < dreal ? p[c] : u32x4{0u, 0u, 0u, 0u});
+  }
 }
 
 // Write one gradient tile: lane l, register i holds row base + 8 (i / 4) + 4 half + i % 4,
 // column 32 nb + l % 32; the factor s of S = s Q K^T is applied here, times
-// row_scale(i) when given.
+// row_scale(i) when given. dreal: the row length in global memory (the
+// 32-column blocks past it belong to a padded head dim and are dropped).
 template <int D, typename RowScale>
 __device__ __forceinline__ void write_grad(float* out, const f32x16 (&acc)[D / 32], size_t bh_rows, int base,
-                                           int n, float s, int lane, RowScale row_scale) {
+                                           int n, float s, int lane, int dreal, RowScale row_scale) {
   const int half = lane >> 5;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     const int row = base + 8 * (i >> 2) + 4 * half + (i & 3);
     if (row < n) {
       const float f = s * row_scale(i);
-      float* o = out + (bh_rows + row) * D + (lane & 31);
+      float* o = out + (bh_rows + row) * dreal + (lane & 31);
 #pragma unroll
-      for (int nb = 0; nb < D / 32; ++nb) o[32 * nb] = acc[nb][i] * f;
+      for (int nb = 0; nb < D / 32; ++nb)
+        if (32 * nb < dreal) o[32 * nb] = acc[nb][i] * f;
     }
   }
 }
 template <int D>
 __device__ __forceinline__ void write_grad(float* out, const f32x16 (&acc)[D / 32], size_t bh_rows, int base,
-                                           int n, float s, int lane) {
-  write_grad<D>(out, acc, bh_rows, base, n, s, lane, [](int) { return 1.f; });
+                                           int n, float s, int lane, int dreal = D) {
+  write_grad<D>(out, acc, bh_rows, base, n, s, lane, dreal, [](int) { return 1.f; });
 }
 
 // ----------------------------------------------------------------------------
 // dQ kernel: workgroup = 128 query rows of one (batch, head), streams key tiles.
 // ----------------------------------------------------------------------------
-template <int DA, int DB, bool CAUSAL, int MODE, int ACT = kActSoftmax>
+template <int DA, int DB, bool CAUSAL, int MODE, int ACT = kActSoftmax, bool PD = false>
 __global__ void __launch_bounds__(kThreads, (BwdCfg<DA, DB, MODE>::MINB))
 kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
                  const uint16_t* __restrict__ Qb, const uint16_t* __restrict__ Kb,
-                 int NQ, int NK, float sa, float sb,
+                 int NQ, int NK, int dra, int drb, float sa, float sb,
                  const float* __restrict__ kl, const float* __restrict__ lse_a,
                  const float* __restrict__ lse_b, const float* __restrict__ g,
                  float* __restrict__ dQa, float* __restrict__ dQb) {
+  // PD: the head dims may be padded (the rows in memory are dra, drb long);
+  // otherwise they are the compile-time ones and the runtime values unused
+  if constexpr (!PD) {
+    dra = DA;
+    drb = DB;
+  }
   using C = BwdCfg<DA, DB, MODE>;
   // Two stages of key tiles as two arrays, so that the compiler can tell
   // which stage each LDS read touches (the loop names each stage's array
@@ -419,8 +431,8 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   const float gsign = FOLD && rs0.g < 0.f ? -1.f : 1.f;
   const RowStats rs = FOLD ? fold_row_stats(rs0) : rs0;
   bf16x8 qa[DA / 16], qb[DB / 16];
-  load_resident<DA>(qa, Qa, (size_t)bh * NQ, myq, NQ, half);
-  load_resident<DB>(qb, Qb, (size_t)bh * NQ, myq, NQ, half);
+  load_resident<DA>(qa, Qa, (size_t)bh * NQ, myq, NQ, half, dra);
+  load_resident<DB>(qb, Qb, (size_t)bh * NQ, myq, NQ, half, drb);
   // complete before the tile loop: a wait for them inside the loop would
   // also wait for the loads of the next tile
   wait_vmem();
@@ -431,9 +443,9 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
 #pragma unroll
   for (int n = 0; n < (C::WANT_B ? DB / 32 : 1); ++n) dqb[n] = zero16();
 
-  const rsrc_t rka = make_rsrc(Ka + (size_t)bh * NK * DA, (uint32_t)NK * DA * 2u);
-  const rsrc_t rkb = make_rsrc(Kb + (size_t)bh * NK * DB, (uint32_t)NK * DB * 2u);
-  const TileDma<C::BS, C::CA, C::CB> dma(tid);
+  const rsrc_t rka = make_rsrc(Ka + (size_t)bh * NK * dra, (uint32_t)NK * dra * 2u);
+  const rsrc_t rkb = make_rsrc(Kb + (size_t)bh * NK * drb, (uint32_t)NK * drb * 2u);
+  const TileDma<C::BS, C::CA, C::CB> dma(tid, dra / 8, drb / 8);
   const int kmax_ok = CAUSAL ? myq + off : NK;
 
   const TrOffsets<DA, DB, MODE> tro(lane);
@@ -457,11 +469,11 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
       bwd_tile<DA, DB, MODE, false, FOLD, ACT>(stage, qa, qb, dqa, dqb, ca, cb, sa, sb, lane, stats, ok, tro);
   };
 
-  if (ntiles > 0) dma.issue(rka, rkb, 0, st0, wave);
+  if (ntiles > 0) dma.issue(rka, rkb, 0, st0, wave, dra, drb);
   wait_vmem();
   __syncthreads();
   auto step = [&](const u32x4* cur, u32x4* nxt, int kt) {
-    if (kt + 1 < ntiles) dma.issue(rka, rkb, (kt + 1) * C::BS, nxt, wave);
+    if (kt + 1 < ntiles) dma.issue(rka, rkb, (kt + 1) * C::BS, nxt, wave, dra, drb);
     tile(cur, kt);
     wait_vmem();
     __syncthreads();
@@ -478,22 +490,28 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
     rsign[i] = __int_as_float(
         __builtin_amdgcn_ds_bpermute(4 * (8 * (i >> 2) + 4 * half + (i & 3)), __float_as_int(gsign)));
   auto row_sign = [&](int i) { return rsign[i]; };
-  if constexpr (C::WANT_B) write_grad<DB>(dQb, dqb, (size_t)bh * NQ, qw, NQ, sb, lane, row_sign);
-  if constexpr (C::WANT_A) write_grad<DA>(dQa, dqa, (size_t)bh * NQ, qw, NQ, sa, lane, row_sign);
+  if constexpr (C::WANT_B) write_grad<DB>(dQb, dqb, (size_t)bh * NQ, qw, NQ, sb, lane, drb, row_sign);
+  if constexpr (C::WANT_A) write_grad<DA>(dQa, dqa, (size_t)bh * NQ, qw, NQ, sa, lane, dra, row_sign);
 }
 
 // ----------------------------------------------------------------------------
 // dK kernel: workgroup = 128 key rows of one (batch, head), streams query tiles
 // together with their row statistics.
 // ----------------------------------------------------------------------------
-template <int DA, int DB, bool CAUSAL, int MODE, int ACT = kActSoftmax>
+template <int DA, int DB, bool CAUSAL, int MODE, int ACT = kActSoftmax, bool PD = false>
 __global__ void __launch_bounds__(kThreads, (BwdCfg<DA, DB, MODE>::MINB))
 kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
                  const uint16_t* __restrict__ Qb, const uint16_t* __restrict__ Kb,
-                 int NQ, int NK, float sa, float sb,
+                 int NQ, int NK, int dra, int drb, float sa, float sb,
                  const float* __restrict__ kl, const float* __restrict__ lse_a,
                  const float* __restrict__ lse_b, const float* __restrict__ g,
                  float* __restrict__ dKa, float* __restrict__ dKb) {
+  // PD: the head dims may be padded (the rows in memory are dra, drb long);
+  // otherwise they are the compile-time ones and the runtime values unused
+  if constexpr (!PD) {
+    dra = DA;
+    drb = DB;
+  }
   using C = BwdCfg<DA, DB, MODE>;
   __shared__ u32x4 st0[C::STAGE];             // two stages of query tiles (two arrays: see the dQ kernel)
   __shared__ u32x4 st1[C::STAGE];
@@ -524,8 +542,8 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   }
 
   bf16x8 ka[DA / 16], kb[DB / 16];
-  load_resident<DA>(ka, Ka, (size_t)bh * NK, myk, NK, half);
-  load_resident<DB>(kb, Kb, (size_t)bh * NK, myk, NK, half);
+  load_resident<DA>(ka, Ka, (size_t)bh * NK, myk, NK, half, dra);
+  load_resident<DB>(kb, Kb, (size_t)bh * NK, myk, NK, half, drb);
   // complete before the tile loop: a wait for them inside the loop would
   // also wait for the loads of the next tile
   wait_vmem();
@@ -536,9 +554,9 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
 #pragma unroll
   for (int n = 0; n < (C::WANT_B ? DB / 32 : 1); ++n) dkb[n] = zero16();
 
-  const rsrc_t rqa = make_rsrc(Qa + (size_t)bh * NQ * DA, (uint32_t)NQ * DA * 2u);
-  const rsrc_t rqb = make_rsrc(Qb + (size_t)bh * NQ * DB, (uint32_t)NQ * DB * 2u);
-  const TileDma<C::BS, C::CA, C::CB> dma(tid);
+  const rsrc_t rqa = make_rsrc(Qa + (size_t)bh * NQ * dra, (uint32_t)NQ * dra * 2u);
+  const rsrc_t rqb = make_rsrc(Qb + (size_t)bh * NQ * drb, (uint32_t)NQ * drb * 2u);
+  const TileDma<C::BS, C::CA, C::CB> dma(tid, dra / 8, drb / 8);
 
   const RowsDma rdma(kl, lse_a, lse_b, g, (size_t)bh * NQ, NQ);
 
@@ -584,7 +602,7 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
     if (wave == 0) stage_row_stats<C::BS, ACT>(raw, t * C::BS, NQ, rdma.has_g, sstat[buf], &sfold[buf], tid);
   };
   if (t_begin < ntq) {
-    dma.issue(rqa, rqb, t_begin * C::BS, st0, wave);
+    dma.issue(rqa, rqb, t_begin * C::BS, st0, wave, dra, drb);
     if (wave == 0) {
       rdma.issue<ACT>(t_begin * C::BS, sraw0, lane);
       if (t_begin + 1 < ntq) rdma.issue<ACT>((t_begin + 1) * C::BS, sraw1, lane);
@@ -595,7 +613,7 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   __syncthreads();
   // rnext holds the row values of tile t + 1; rfree receives those of t + 2
   auto step = [&](const u32x4* cur, u32x4* nxt, float (*rnext)[64], float (*rfree)[64], int t, int buf) {
-    if (t + 1 < ntq) dma.issue(rqa, rqb, (t + 1) * C::BS, nxt, wave);
+    if (t + 1 < ntq) dma.issue(rqa, rqb, (t + 1) * C::BS, nxt, wave, dra, drb);
     if (wave == 0 && t + 2 < ntq) rdma.issue<ACT>((t + 2) * C::BS, rfree, lane);
     if (t + 1 < ntq) stats_in(t + 1, rnext, buf ^ 1);
     tile(cur, buf, t);
@@ -607,8 +625,8 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
     if (t + 1 < ntq) step(st1, st0, sraw0, sraw1, t + 1, 1);
   }
 
-  if constexpr (C::WANT_B) write_grad<DB>(dKb, dkb, (size_t)bh * NK, kw, NK, sb, lane);
-  if constexpr (C::WANT_A) write_grad<DA>(dKa, dka, (size_t)bh * NK, kw, NK, sa, lane);
+  if constexpr (C::WANT_B) write_grad<DB>(dKb, dkb, (size_t)bh * NK, kw, NK, sb, lane, drb);
+  if constexpr (C::WANT_A) write_grad<DA>(dKa, dka, (size_t)bh * NK, kw, NK, sa, lane, dra);
 }
 
 }  // namespace streamkl

@@ -188,7 +188,23 @@ __device__ __forceinline__ void barrier_no_fence() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
-// CB = 0 stages rows of a single matrix.
+// Head dims that are not a multiple of 64 (32, 96, 160, 224) run the kernels
+// of the next multiple of 64: in LDS and in registers a row keeps its
+// compile-time width, and the chunks past the row's real length are zeros.
+// A staging lane whose chunk lies past the real length points its load at
+// kOutOfSlab, an offset beyond every slab (a bf16 slab of one head is below
+// 2^31 bytes, and tile offsets stay below 2^31 too, so the sum does not
+// wrap): the buffer range check turns the load into zeros.
+constexpr uint32_t kOutOfSlab = 0x80000000u;
+
+// Byte offset of logical chunk c of tile row r in a global slab whose rows
+// hold creal 16-byte chunks, or kOutOfSlab for a padding chunk.
+__device__ __forceinline__ uint32_t slab_chunk_offset(int r, int c, int creal) {
+  return c < creal ? (uint32_t)(r * creal + c) * 16u : kOutOfSlab;
+}
+
+// CB = 0 stages rows of a single matrix. creal_a, creal_b: 16-byte chunks
+// per row in global memory (CA, CB unless the head dim is padded).
 template <int R, int CA, int CB, int NT = kThreads>
 struct TileDma {
   static constexpr int NCH = R * (CA + CB) / NT;
@@ -197,27 +213,29 @@ struct TileDma {
   static_assert(CB == 0 || NCH > NCH_A, "second matrix");
   uint32_t voff[NCH];   // byte offset (from the tile's first row) of the chunk this lane fetches
 
-  __device__ __forceinline__ explicit TileDma(int tid) {
+  __device__ __forceinline__ explicit TileDma(int tid, int creal_a = CA, int creal_b = CB) {
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
       const int p = tid + NT * i;
       if (i < NCH_A) {
         const int r = p / CA, c = (p - r * CA) ^ swz<CA>(r);
-        voff[i] = (uint32_t)(r * CA + c) * 16u;
+        voff[i] = slab_chunk_offset(r, c, creal_a);
       } else if constexpr (CB > 0) {
         const int pp = p - R * CA;
         const int r = pp / CB, c = (pp - r * CB) ^ swz<CB>(r);
-        voff[i] = (uint32_t)(r * CB + c) * 16u;
+        voff[i] = slab_chunk_offset(r, c, creal_b);
       }
     }
   }
 
-  // Rows row0 .. row0 + R - 1 of A and B into `stage` (R * (CA + CB) chunks).
-  // The row offset goes into the per-lane offset, which the buffer range
-  // check covers (the scalar offset is not range checked).
-  __device__ __forceinline__ void issue(rsrc_t ra, rsrc_t rb, int row0, u32x4* stage, int wave) const {
+  // Rows row0 .. row0 + R - 1 of A and B into `stage` (R * (CA + CB) chunks);
+  // dra, drb: the rows' lengths in global memory (elements). The row offset
+  // goes into the per-lane offset, which the buffer range check covers (the
+  // scalar offset is not range checked).
+  __device__ __forceinline__ void issue(rsrc_t ra, rsrc_t rb, int row0, u32x4* stage, int wave, int dra = 8 * CA,
+                                        int drb = 8 * CB) const {
 #if defined(__HIP_DEVICE_COMPILE__)   // the host pass never runs this; keep its builtins out of it
-    const uint32_t base_a = (uint32_t)row0 * CA * 16u, base_b = (uint32_t)row0 * CB * 16u;
+    const uint32_t base_a = (uint32_t)row0 * (uint32_t)dra * 2u, base_b = (uint32_t)row0 * (uint32_t)drb * 2u;
 #pragma unroll
     for (int i = 0; i < NCH_A; ++i)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(stage + NT * i + 64 * wave), 16,
@@ -261,21 +279,22 @@ struct PadTileDma {
   uint32_t voff[NCH];
 
   template <int CPR, int P>
-  __device__ __forceinline__ static uint32_t chunk_of(int s) {
+  __device__ __forceinline__ static uint32_t chunk_of(int s, int creal) {
     const int r = s / P, p = s - r * P - PadRows<CPR>::rot(r);
     const int c = (p < 0 || p >= CPR) ? 0 : (p < CPR / 2 ? 2 * p : 2 * (p - CPR / 2) + 1);
-    return (uint32_t)(r * CPR + c) * 16u;
+    return slab_chunk_offset(r, c, creal);
   }
-  __device__ __forceinline__ explicit PadTileDma(int tid) {
+  __device__ __forceinline__ explicit PadTileDma(int tid, int creal_a = CA, int creal_b = CB) {
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
       const int p = tid + NT * i;
-      voff[i] = i < NCH_A ? chunk_of<CA, PA>(p) : chunk_of<CB, PB>(p - R * PA);
+      voff[i] = i < NCH_A ? chunk_of<CA, PA>(p, creal_a) : chunk_of<CB, PB>(p - R * PA, creal_b);
     }
   }
-  __device__ __forceinline__ void issue(rsrc_t ra, rsrc_t rb, int row0, u32x4* stage, int wave) const {
+  __device__ __forceinline__ void issue(rsrc_t ra, rsrc_t rb, int row0, u32x4* stage, int wave, int dra = 8 * CA,
+                                        int drb = 8 * CB) const {
 #if defined(__HIP_DEVICE_COMPILE__)
-    const uint32_t base_a = (uint32_t)row0 * CA * 16u, base_b = (uint32_t)row0 * CB * 16u;
+    const uint32_t base_a = (uint32_t)row0 * (uint32_t)dra * 2u, base_b = (uint32_t)row0 * (uint32_t)drb * 2u;
 #pragma unroll
     for (int i = 0; i < NCH_A; ++i)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(stage + NT * i + 64 * wave), 16,

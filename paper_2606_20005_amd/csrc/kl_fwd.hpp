@@ -187,14 +187,18 @@ __device__ __forceinline__ void fwd_logits(const u32x4* stage, const bf16x8 (&qa
 }
 
 // Q rows of this lane as MFMA B operands: chunk 2 * ks + half of row myq.
+// dreal: the row length in global memory (D, or less for a padded head dim:
+// the chunks past it are zeros).
 template <int D>
 __device__ __forceinline__ void load_q_operands(bf16x8 (&q)[D / 16], const uint16_t* Q, size_t bh, int NQ, int myq,
-                                                int half) {
+                                                int half, int dreal) {
   const bool okq = myq < NQ;
-  const u32x4* p = reinterpret_cast<const u32x4*>(Q + (bh * NQ + (okq ? myq : 0)) * D);
+  const u32x4* p = reinterpret_cast<const u32x4*>(Q + (bh * NQ + (okq ? myq : 0)) * dreal);
 #pragma unroll
-  for (int ks = 0; ks < D / 16; ++ks)
-    q[ks] = __builtin_bit_cast(bf16x8, okq ? p[2 * ks + half] : u32x4{0u, 0u, 0u, 0u});
+  for (int ks = 0; ks < D / 16; ++ks) {
+    const int c = 2 * ks + half;
+    q[ks] = __builtin_bit_cast(bf16x8, okq && 8 * c < dreal ? p[c] : u32x4{0u, 0u, 0u, 0u});
+  }
 }
 
 // Five row statistics with the maxima scaled to the base-2 exponent domain
@@ -416,8 +420,9 @@ template <class C, bool CAUSAL, class Rows = SoftmaxRows>
 __device__ __forceinline__ typename Rows::Partial fwd_pass(u32x4* st0, u32x4* st1, float* tot,
                                                            const uint16_t* __restrict__ Qa,
                                                const uint16_t* __restrict__ Ka, const uint16_t* __restrict__ Qb,
-                                               const uint16_t* __restrict__ Kb, int NQ, int NK, float ca, float cb,
-                                               int bh, int q0, int t_begin, int t_end, int& myq) {
+                                               const uint16_t* __restrict__ Kb, int NQ, int NK, int dra, int drb,
+                                               float ca, float cb, int bh, int q0, int t_begin, int t_end,
+                                               int& myq) {
   constexpr int DA = C::DA, DB = C::DB, BK = C::BK;
   static_assert(C::NSTAGE == 2, "the tile loop names two stage arrays");
   const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
@@ -437,15 +442,15 @@ __device__ __forceinline__ typename Rows::Partial fwd_pass(u32x4* st0, u32x4* st
   const int kcm = CAUSAL ? myq + off : NK;
 
   bf16x8 qa[DA / 16], qb[DB / 16];
-  load_q_operands<DA>(qa, Qa, (size_t)bh, NQ, myq, half);
-  load_q_operands<DB>(qb, Qb, (size_t)bh, NQ, myq, half);
+  load_q_operands<DA>(qa, Qa, (size_t)bh, NQ, myq, half, dra);
+  load_q_operands<DB>(qb, Qb, (size_t)bh, NQ, myq, half, drb);
 
-  const rsrc_t rka = make_rsrc(Ka + (size_t)bh * NK * DA, (uint32_t)NK * DA * 2u);
-  const rsrc_t rkb = make_rsrc(Kb + (size_t)bh * NK * DB, (uint32_t)NK * DB * 2u);
+  const rsrc_t rka = make_rsrc(Ka + (size_t)bh * NK * dra, (uint32_t)NK * dra * 2u);
+  const rsrc_t rkb = make_rsrc(Kb + (size_t)bh * NK * drb, (uint32_t)NK * drb * 2u);
   using Dma = typename std::conditional<C::PAD, PadTileDma<BK, C::CA, C::CB, C::DMA_NT>,
                                         TileDma<BK, C::CA, C::CB, C::DMA_NT>>::type;
   const bool streamer = wave < C::DMA_NT / 64;
-  const Dma dma(streamer ? tid : 0);
+  const Dma dma(streamer ? tid : 0, dra / 8, drb / 8);
   // operand bases of the row-padded layout (unused otherwise)
   const int base_a = C::PAD ? PadRows<C::CA>::base(lane & 31, half) : 0;
   const int base_b = C::PAD ? PadRows<C::CB>::base(lane & 31, half) : 0;
@@ -453,7 +458,7 @@ __device__ __forceinline__ typename Rows::Partial fwd_pass(u32x4* st0, u32x4* st
   bool have_total = false;   // uniform: whether tot holds a chunk yet
 
   if (t_begin < t_end && streamer) {
-    dma.issue(rka, rkb, t_begin * BK, st0, wave);
+    dma.issue(rka, rkb, t_begin * BK, st0, wave, dra, drb);
     wait_vmem();   // tile t_begin
   }
   barrier_no_fence();
@@ -462,7 +467,7 @@ __device__ __forceinline__ typename Rows::Partial fwd_pass(u32x4* st0, u32x4* st
   // the compiler can tell that a tile's reads never touch the stage being
   // loaded (and inserts no wait for those loads).
   auto step = [&](const u32x4* cur, u32x4* nxt, int t) {
-    if (streamer) dma.issue(rka, rkb, (t + 1) * BK, nxt, wave);
+    if (streamer) dma.issue(rka, rkb, (t + 1) * BK, nxt, wave, dra, drb);
     if (t <= wt.tlast) {
       f32x16 sa, sb;
       fwd_logits<DA, DB, C::PAD>(cur, qa, qb, sa, sb, lane, base_a, base_b);
@@ -490,12 +495,18 @@ __device__ __forceinline__ typename Rows::Partial fwd_pass(u32x4* st0, u32x4* st
 }
 
 // Whole key range per workgroup: grid B*H * ceil(N_Q / BQ).
-template <class C, bool CAUSAL>
+template <class C, bool CAUSAL, bool PD = false>
 __global__ void __launch_bounds__(C::NT, C::WAVES_PER_SIMD)
 kl_fwd_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
               const uint16_t* __restrict__ Qb, const uint16_t* __restrict__ Kb,
-              int NQ, int NK, float ca, float cb,
+              int NQ, int NK, int dra, int drb, float ca, float cb,
               float* __restrict__ kl, float* __restrict__ lse_a, float* __restrict__ lse_b) {
+  // PD: the head dims may be padded (the rows in memory are dra, drb long);
+  // otherwise they are the compile-time ones and the runtime values unused
+  if constexpr (!PD) {
+    dra = C::DA;
+    drb = C::DB;
+  }
   __shared__ u32x4 st0[C::STAGE];
   __shared__ u32x4 st1[C::STAGE];
   __shared__ float tot[SoftmaxRows::NTOT * C::NT];
@@ -506,18 +517,25 @@ kl_fwd_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
   if (CAUSAL) qt = TQ - 1 - qt;   // longest rows first
   int myq;
   const RowPartial p =
-      fwd_pass<C, CAUSAL>(st0, st1, tot, Qa, Ka, Qb, Kb, NQ, NK, ca, cb, bh, qt * C::BQ, 0, 1 << 30, myq);
+      fwd_pass<C, CAUSAL>(st0, st1, tot, Qa, Ka, Qb, Kb, NQ, NK, dra, drb, ca, cb, bh, qt * C::BQ, 0, 1 << 30,
+                          myq);
   if ((threadIdx.x & 32) == 0 && myq < NQ) write_row(p, (size_t)bh * NQ + myq, kl, lse_a, lse_b);
 }
 
 // Forward of the sigmoid-score divergence (see SigmoidRows): the same tile
 // loop over the whole key range, grid B*H * ceil(N_Q / BQ).
-template <class C, bool CAUSAL>
+template <class C, bool CAUSAL, bool PD = false>
 __global__ void __launch_bounds__(C::NT, C::WAVES_PER_SIMD)
 kl_fwd_sigmoid_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
                       const uint16_t* __restrict__ Qb, const uint16_t* __restrict__ Kb,
-                      int NQ, int NK, float ca, float cb,
+                      int NQ, int NK, int dra, int drb, float ca, float cb,
                       float* __restrict__ kl, float* __restrict__ mass_a, float* __restrict__ mass_b) {
+  // PD: the head dims may be padded (the rows in memory are dra, drb long);
+  // otherwise they are the compile-time ones and the runtime values unused
+  if constexpr (!PD) {
+    dra = C::DA;
+    drb = C::DB;
+  }
   __shared__ u32x4 st0[C::STAGE];
   __shared__ u32x4 st1[C::STAGE];
   __shared__ float tot[SigmoidRows::NTOT * C::NT];
@@ -527,8 +545,8 @@ kl_fwd_sigmoid_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restric
   int qt = logical - bh * TQ;
   if (CAUSAL) qt = TQ - 1 - qt;   // longest rows first
   int myq;
-  const SigmoidPartial p = fwd_pass<C, CAUSAL, SigmoidRows>(st0, st1, tot, Qa, Ka, Qb, Kb, NQ, NK, ca, cb, bh,
-                                                            qt * C::BQ, 0, 1 << 30, myq);
+  const SigmoidPartial p = fwd_pass<C, CAUSAL, SigmoidRows>(st0, st1, tot, Qa, Ka, Qb, Kb, NQ, NK, dra, drb, ca, cb,
+                                                            bh, qt * C::BQ, 0, 1 << 30, myq);
   if ((threadIdx.x & 32) == 0 && myq < NQ) write_row_sigmoid(p, (size_t)bh * NQ + myq, kl, mass_a, mass_b);
 }
 
@@ -536,11 +554,17 @@ kl_fwd_sigmoid_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restric
 // (head, query tile, w) covers key tiles [w * chunk, (w + 1) * chunk) and
 // writes the five row statistics to part[k][w][B*H*N_Q], k = (m_a, l_a, m_b,
 // l_b, acc), maxima in the base-2 domain.
-template <class C, bool CAUSAL>
+template <class C, bool CAUSAL, bool PD = false>
 __global__ void __launch_bounds__(C::NT, C::WAVES_PER_SIMD)
 kl_fwd_partial_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
                       const uint16_t* __restrict__ Qb, const uint16_t* __restrict__ Kb,
-                      int NQ, int NK, float ca, float cb, int W, int chunk, float* __restrict__ part) {
+                      int NQ, int NK, int dra, int drb, float ca, float cb, int W, int chunk, float* __restrict__ part) {
+  // PD: the head dims may be padded (the rows in memory are dra, drb long);
+  // otherwise they are the compile-time ones and the runtime values unused
+  if constexpr (!PD) {
+    dra = C::DA;
+    drb = C::DB;
+  }
   __shared__ u32x4 st0[C::STAGE];
   __shared__ u32x4 st1[C::STAGE];
   __shared__ float tot[SoftmaxRows::NTOT * C::NT];
@@ -551,8 +575,8 @@ kl_fwd_partial_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restric
   const int bh = rest / TQ;
   const int qt = rest - bh * TQ;
   int myq;
-  const RowPartial p = fwd_pass<C, CAUSAL>(st0, st1, tot, Qa, Ka, Qb, Kb, NQ, NK, ca, cb, bh, qt * C::BQ, w * chunk,
-                                           (w + 1) * chunk, myq);
+  const RowPartial p = fwd_pass<C, CAUSAL>(st0, st1, tot, Qa, Ka, Qb, Kb, NQ, NK, dra, drb, ca, cb, bh, qt * C::BQ,
+                                           w * chunk, (w + 1) * chunk, myq);
   if ((threadIdx.x & 32) == 0 && myq < NQ) {
     const size_t rows = (size_t)gridDim.x / W / TQ * NQ;   // B*H*N_Q
     const size_t ri = (size_t)w * rows + (size_t)bh * NQ + myq;
@@ -610,6 +634,11 @@ using FwdCfg = typename std::conditional<(DA + DB <= 256), FwdTraits<DA, DB, 2, 
 // the default key-tile layout, two workgroups per CU.
 template <int DA, int DB>
 using FwdCausalSmallCfg = FwdTraits<DA, DB, 2, 2, 4, true>;
+
+// Padded head dims (32, 96, 160, 224 run as 64, 128, 192, 256): one
+// configuration for every shape, four waves and 128 rows per workgroup.
+template <int DA, int DB>
+using FwdPadDimCfg = FwdTraits<DA, DB, 2, (DA + DB <= 256) ? 2 : 1, 4, true>;
 
 // Few query rows per head (decode-like shapes): NW waves per workgroup; four
 // one-wave or two four-wave workgroups per CU (one for wide heads).

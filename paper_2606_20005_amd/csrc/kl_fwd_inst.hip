@@ -6,20 +6,20 @@ namespace streamkl {
 
 // Waves per workgroup follow the query rows of a head: one wave for at most 32
 // rows, four for at most 128, otherwise the default configuration.
-template <int DA, int DB, bool CAUSAL, class C>
+template <int DA, int DB, bool CAUSAL, class C, bool PD = false>
 static hipError_t run_cfg(const FwdArgs& a, int W, float* part) {
   const int tq = (a.NQ + C::BQ - 1) / C::BQ;
   if (W <= 1) {
     const dim3 grid((unsigned)((long long)a.BH * tq));
-    hipLaunchKernelGGL((kl_fwd_kernel<C, CAUSAL>), grid, dim3(C::NT), 0, a.stream,
-                       a.Qa, a.Ka, a.Qb, a.Kb, a.NQ, a.NK, a.ca, a.cb, a.kl, a.lse_a, a.lse_b);
+    hipLaunchKernelGGL((kl_fwd_kernel<C, CAUSAL, PD>), grid, dim3(C::NT), 0, a.stream,
+                       a.Qa, a.Ka, a.Qb, a.Kb, a.NQ, a.NK, a.dra, a.drb, a.ca, a.cb, a.kl, a.lse_a, a.lse_b);
     return hipGetLastError();
   }
   const int nkt = (a.NK + C::BK - 1) / C::BK;
   const int chunk = (nkt + W - 1) / W;
   const dim3 grid((unsigned)((long long)a.BH * tq * W));
-  hipLaunchKernelGGL((kl_fwd_partial_kernel<C, CAUSAL>), grid, dim3(C::NT), 0, a.stream,
-                     a.Qa, a.Ka, a.Qb, a.Kb, a.NQ, a.NK, a.ca, a.cb, W, chunk, part);
+  hipLaunchKernelGGL((kl_fwd_partial_kernel<C, CAUSAL, PD>), grid, dim3(C::NT), 0, a.stream,
+                     a.Qa, a.Ka, a.Qb, a.Kb, a.NQ, a.NK, a.dra, a.drb, a.ca, a.cb, W, chunk, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t rows = (size_t)a.BH * a.NQ;
@@ -31,6 +31,7 @@ static hipError_t run_cfg(const FwdArgs& a, int W, float* part) {
 
 template <int DA, int DB, bool CAUSAL>
 static hipError_t run_fwd(const FwdArgs& a, int W, float* part) {
+  if (a.dra != DA || a.drb != DB) return run_cfg<DA, DB, CAUSAL, FwdPadDimCfg<DA, DB>, true>(a, W, part);
   switch (fwd_shape(DA, DB, a.NQ, a.BH, CAUSAL)) {
     case FwdShape::kOneWave: return run_cfg<DA, DB, CAUSAL, FwdSmallCfg<DA, DB, 1>>(a, W, part);
     case FwdShape::kFourWaves:
@@ -46,7 +47,8 @@ static hipError_t run_fwd(const FwdArgs& a, int W, float* part) {
 
 int fwd_merge_rows_per_workgroup() { return kMergeRowsPerBlock; }
 
-int fwd_rows_per_workgroup(int da, int db, int n_q, long long bh, bool causal) {
+int fwd_rows_per_workgroup(int da, int db, int n_q, long long bh, bool causal, bool padded) {
+  if (padded) return 128;   // FwdPadDimCfg
   switch (fwd_shape(da, db, n_q, bh, causal)) {
     case FwdShape::kOneWave: return 32;
     case FwdShape::kFourWaves:

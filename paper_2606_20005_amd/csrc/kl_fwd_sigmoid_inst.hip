@@ -6,17 +6,18 @@
 
 namespace streamkl {
 
-template <int DA, int DB, bool CAUSAL, class C>
+template <int DA, int DB, bool CAUSAL, class C, bool PD = false>
 static hipError_t run_sig(const FwdArgs& a) {
   const int tq = (a.NQ + C::BQ - 1) / C::BQ;
   const dim3 grid((unsigned)((long long)a.BH * tq));
-  hipLaunchKernelGGL((kl_fwd_sigmoid_kernel<C, CAUSAL>), grid, dim3(C::NT), 0, a.stream,
-                     a.Qa, a.Ka, a.Qb, a.Kb, a.NQ, a.NK, a.ca, a.cb, a.kl, a.lse_a, a.lse_b);
+  hipLaunchKernelGGL((kl_fwd_sigmoid_kernel<C, CAUSAL, PD>), grid, dim3(C::NT), 0, a.stream,
+                     a.Qa, a.Ka, a.Qb, a.Kb, a.NQ, a.NK, a.dra, a.drb, a.ca, a.cb, a.kl, a.lse_a, a.lse_b);
   return hipGetLastError();
 }
 
 template <int DA, int DB, bool CAUSAL>
 static hipError_t run_fwd_sig(const FwdArgs& a) {
+  if (a.dra != DA || a.drb != DB) return run_sig<DA, DB, CAUSAL, FwdPadDimCfg<DA, DB>, true>(a);
   switch (fwd_shape(DA, DB, a.NQ, a.BH, CAUSAL)) {
     case FwdShape::kOneWave: return run_sig<DA, DB, CAUSAL, FwdSmallCfg<DA, DB, 1>>(a);
     case FwdShape::kFourWaves:

@@ -9,9 +9,14 @@ namespace streamkl {
 
 // Arguments after the host has resolved the KL direction: "a" is the
 // distribution in the first KL slot, "b" the one in the second.
+// Head dims: the kernels are instantiated for multiples of 64 (da, db of the
+// launch functions); dra, drb are the row lengths of the tensors in memory,
+// equal to da, db or, for 32, 96, 160 and 224, 32 less (the kernels treat
+// the missing columns as zeros).
 struct FwdArgs {
   const uint16_t *Qa, *Ka, *Qb, *Kb;
   int BH, NQ, NK;
+  int dra, drb;
   float ca, cb;                 // s * log2(e)
   float *kl, *lse_a, *lse_b;
   hipStream_t stream;
@@ -20,6 +25,7 @@ struct FwdArgs {
 struct BwdArgs {
   const uint16_t *Qa, *Ka, *Qb, *Kb;
   int BH, NQ, NK;
+  int dra, drb;
   float sa, sb;
   const float *kl, *lse_a, *lse_b, *g;
   float *dQa, *dQb, *dKa, *dKb;
@@ -35,9 +41,9 @@ hipError_t launch_fwd(int da, int db, bool causal, const FwdArgs& a, int W, floa
 // Sigmoid-score forward (one pass): kl, and the row masses of the first and
 // second slot in lse_a / lse_b (either may be null). ca, cb are s * log2(e).
 hipError_t launch_fwd_sigmoid(int da, int db, bool causal, const FwdArgs& a);
-// Query rows per workgroup of the forward for these head dims, rows per head,
-// number of heads and mask.
-int fwd_rows_per_workgroup(int da, int db, int n_q, long long bh, bool causal);
+// Query rows per workgroup of the forward for these (kernel) head dims, rows
+// per head, number of heads and mask; padded: the real dims are narrower.
+int fwd_rows_per_workgroup(int da, int db, int n_q, long long bh, bool causal, bool padded);
 // Rows per workgroup of the split-K merge.
 int fwd_merge_rows_per_workgroup();
 hipError_t launch_bwd_dq(int da, int db, bool causal, int mode, const BwdArgs& a);

@@ -17,7 +17,13 @@ using streamkl::FwdArgs;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr long long kMaxGrid = 0x7fffffffLL;
 
-bool supported_dim(int d) { return d == 64 || d == 128 || d == 192 || d == 256; }
+// Head dims: multiples of 32 up to 256. The kernels exist for multiples of
+// 64; 32, 96, 160 and 224 run those of the next multiple of 64 with the real
+// row length passed along (the extra columns read as zeros and gradients are
+// written only for the real ones). The fused backward keeps to multiples of
+// 64 (its end-of-tile wait counts every dQ atomic of the tile).
+bool supported_dim(int d) { return d >= 32 && d <= 256 && d % 32 == 0; }
+int kernel_dim(int d) { return (d + 63) / 64 * 64; }
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 bool scale_ok(float s) { return std::isfinite(s) && s > 0.f; }
 
@@ -111,7 +117,8 @@ int fwd_common(const void* Q1, const void* K1, const void* Q2, const void* K2, i
   if (splits < 1) return STREAMKL_ERR_INVALID_ARG;
   if (splits > 1) {
     const long long rows = (long long)B * H * N_Q;
-    const int bq = streamkl::fwd_rows_per_workgroup(d1, d2, N_Q, (long long)B * H, causal == 1);
+    const int bq = streamkl::fwd_rows_per_workgroup(kernel_dim(d1), kernel_dim(d2), N_Q, (long long)B * H,
+                                                    causal == 1, d1 % 64 != 0 || d2 % 64 != 0);
     const long long grid = (long long)B * H * ((N_Q + bq - 1) / bq) * splits;
     const long long merge_grid =
         (rows + streamkl::fwd_merge_rows_per_workgroup() - 1) / streamkl::fwd_merge_rows_per_workgroup();
@@ -139,13 +146,15 @@ int fwd_common(const void* Q1, const void* K1, const void* Q2, const void* K2, i
   a.BH = B * H;
   a.NQ = N_Q;
   a.NK = N_K;
+  a.dra = rev ? d2 : d1;
+  a.drb = rev ? d1 : d2;
   a.ca = (rev ? s2 : s1) * kLog2e;
   a.cb = (rev ? s1 : s2) * kLog2e;
   a.kl = kl;
   a.lse_a = rev ? lse2 : lse1;
   a.lse_b = rev ? lse1 : lse2;
   a.stream = stream;
-  return hip_status(streamkl::launch_fwd(rev ? d2 : d1, rev ? d1 : d2, causal == 1, a, splits,
+  return hip_status(streamkl::launch_fwd(kernel_dim(a.dra), kernel_dim(a.drb), causal == 1, a, splits,
                                          static_cast<float*>(workspace)));
 }
 
@@ -179,13 +188,15 @@ extern "C" int streamkl_fwd_act(const void* Q1, const void* K1, const void* Q2, 
   a.BH = B * H;
   a.NQ = N_Q;
   a.NK = N_K;
+  a.dra = rev ? d2 : d1;
+  a.drb = rev ? d1 : d2;
   a.ca = (rev ? s2 : s1) * kLog2e;
   a.cb = (rev ? s1 : s2) * kLog2e;
   a.kl = kl;
   a.lse_a = rev ? stat2 : stat1;
   a.lse_b = rev ? stat1 : stat2;
   a.stream = stream;
-  return hip_status(streamkl::launch_fwd_sigmoid(rev ? d2 : d1, rev ? d1 : d2, causal == 1, a));
+  return hip_status(streamkl::launch_fwd_sigmoid(kernel_dim(a.dra), kernel_dim(a.drb), causal == 1, a));
 }
 
 extern "C" int streamkl_fwd_split(const void* Q1, const void* K1, const void* Q2, const void* K2, int B, int H,
@@ -213,7 +224,8 @@ extern "C" int streamkl_fwd_split_count(int B, int H, int N_Q, int N_K, int d1, 
   if (B < 0 || H < 0 || N_Q < 0 || N_K < 0) return 0;
   if (!supported_dim(d1) || !supported_dim(d2)) return 0;
   constexpr long long kTarget = 512;   // two workgroups per CU on 256 CUs
-  const int bq = streamkl::fwd_rows_per_workgroup(d1, d2, N_Q, (long long)B * H, false);
+  const int bq = streamkl::fwd_rows_per_workgroup(kernel_dim(d1), kernel_dim(d2), N_Q, (long long)B * H, false,
+                                                  d1 % 64 != 0 || d2 % 64 != 0);
   const long long base = (long long)B * H * ((N_Q + bq - 1) / bq);
   if (base == 0 || base >= kTarget) return 1;
   const long long tiles = (N_K + 31LL) / 32;
@@ -260,10 +272,12 @@ int bwd_common(const void* Q1, const void* K1, const void* Q2, const void* K2, i
   int st = check_common(Q1, K1, Q2, K2, B, H, N_Q, N_K, d1, d2, s1, s2, causal, direction, &empty);
   if (st != STREAMKL_OK) return st;
   const bool rev = direction == STREAMKL_KL_REV;
-  const int da = rev ? d2 : d1, db = rev ? d1 : d2;
+  const int da = rev ? d2 : d1, db = rev ? d1 : d2;                  // real head dims
+  const int kda = kernel_dim(da), kdb = kernel_dim(db);              // the kernels' head dims
   const BwdModes m = bwd_modes(rev, dQ1, dK1, dQ2, dK2);
   const bool sig = act == STREAMKL_ACT_SIGMOID;
-  const bool fused_ok = !sig && m.q != 0 && streamkl::bwd_fused_fits(da, db, m.q | m.k);
+  const bool fused_ok =
+      !sig && m.q != 0 && da == kda && db == kdb && streamkl::bwd_fused_fits(kda, kdb, m.q | m.k);
   if (strategy == STREAMKL_BWD_FUSED && m.q != 0 && !fused_ok) return STREAMKL_ERR_UNSUPPORTED;
   const bool fused = fused_ok && (strategy == STREAMKL_BWD_FUSED ||
                                   (strategy == STREAMKL_BWD_AUTO && fused_preferred(N_Q, N_K)));
@@ -289,6 +303,8 @@ int bwd_common(const void* Q1, const void* K1, const void* Q2, const void* K2, i
   a.BH = (int)bh;
   a.NQ = N_Q;
   a.NK = N_K;
+  a.dra = da;
+  a.drb = db;
   a.sa = rev ? s2 : s1;
   a.sb = rev ? s1 : s2;
   a.kl = kl;
@@ -311,11 +327,11 @@ int bwd_common(const void* Q1, const void* K1, const void* Q2, const void* K2, i
     // dQ accumulates atomically over key blocks: start from zero
     e = zero_fill(a.dQa, (size_t)bh * N_Q * da, stream);
     if (e == hipSuccess) e = zero_fill(a.dQb, (size_t)bh * N_Q * db, stream);
-    if (e == hipSuccess) e = streamkl::launch_bwd_fused(da, db, causal == 1, m.q | m.k, a);
+    if (e == hipSuccess) e = streamkl::launch_bwd_fused(kda, kdb, causal == 1, m.q | m.k, a);
     return hip_status(e);
   }
-  if (m.q) e = streamkl::launch_bwd_dq(da, db, causal == 1, m.q, a);
-  if (e == hipSuccess && m.k && N_K > 0) e = streamkl::launch_bwd_dk(da, db, causal == 1, m.k, a);
+  if (m.q) e = streamkl::launch_bwd_dq(kda, kdb, causal == 1, m.q, a);
+  if (e == hipSuccess && m.k && N_K > 0) e = streamkl::launch_bwd_dk(kda, kdb, causal == 1, m.k, a);
   return hip_status(e);
 }
 
@@ -355,7 +371,8 @@ extern "C" int streamkl_bwd_choose(int B, int H, int N_Q, int N_K, int d1, int d
   const bool rev = direction == STREAMKL_KL_REV;
   const BwdModes m = bwd_modes(rev, grads & STREAMKL_GRAD_DQ1, grads & STREAMKL_GRAD_DK1, grads & STREAMKL_GRAD_DQ2,
                                grads & STREAMKL_GRAD_DK2);
-  const bool fused_ok = m.q != 0 && streamkl::bwd_fused_fits(rev ? d2 : d1, rev ? d1 : d2, m.q | m.k);
+  const int da = rev ? d2 : d1, db = rev ? d1 : d2;
+  const bool fused_ok = m.q != 0 && da % 64 == 0 && db % 64 == 0 && streamkl::bwd_fused_fits(da, db, m.q | m.k);
   return fused_ok && fused_preferred(N_Q, N_K) ? STREAMKL_BWD_FUSED : STREAMKL_BWD_SEPARATE;
 }
 
@@ -363,7 +380,8 @@ extern "C" const char* streamkl_strerror(int status) {
   switch (status) {
     case STREAMKL_OK: return "success";
     case STREAMKL_ERR_INVALID_ARG: return "invalid argument (null pointer, negative extent, flag, scale or alignment)";
-    case STREAMKL_ERR_UNSUPPORTED: return "unsupported configuration (head dim not in {64,128,192,256} or extent too large)";
+    case STREAMKL_ERR_UNSUPPORTED:
+      return "unsupported configuration (head dim not a multiple of 32 in [32, 256], or extent too large)";
     case STREAMKL_ERR_HIP: return "HIP runtime rejected a kernel launch";
     case STREAMKL_ERR_SCRATCH_LIMIT:
       return "request needs more partial-statistics space than the allocation-free forward's static scratch holds";

@@ -37,7 +37,7 @@ def test_version_and_strerror(sk):
     for st in range(5):
         assert sk.lib.streamkl_strerror(st)
     assert b"unknown" in sk.lib.streamkl_strerror(99)
-    assert [d for d in range(0, 300) if sk.supported_head_dim(d)] == [64, 128, 192, 256]
+    assert [d for d in range(0, 300) if sk.supported_head_dim(d)] == list(range(32, 257, 32))
 
 
 FAKE = ctypes.c_void_p(0x100000)        # 16-byte aligned, never dereferenced on error paths
@@ -69,7 +69,7 @@ def bwd_call(sk, **kw):
     (dict(B=-1), 1), (dict(NQ=-3), 1), (dict(NK=-1), 1), (dict(causal=2), 1), (dict(direction=5), 1),
     (dict(s1=0.0), 1), (dict(s2=-0.5), 1), (dict(s1=float("inf")), 1), (dict(s2=float("nan")), 1),
     (dict(Q1=MIS), 1), (dict(K1=MIS), 1),
-    (dict(d1=96), 2), (dict(d2=32), 2), (dict(d1=512), 2), (dict(B=70000, H=70000), 2),
+    (dict(d1=80), 2), (dict(d2=16), 2), (dict(d2=288), 2), (dict(d1=512), 2), (dict(B=70000, H=70000), 2),
     (dict(B=0), 0), (dict(H=0), 0), (dict(NQ=0, Q1=None, Q2=None, kl=None, lse1=None, lse2=None,
                                           dQ2=None, dK2=None, dK1=FAKE), None),
 ])
@@ -95,7 +95,7 @@ def bwd_ex_call(sk, strategy=0, **kw):
 @pytest.mark.parametrize("kw,expect", [
     (dict(Q1=None), 1), (dict(kl=None), 1), (dict(NK=-1), 1), (dict(causal=2), 1), (dict(s2=0.0), 1),
     (dict(K2=MIS), 1), (dict(dQ2=ctypes.c_void_p(0x100002)), 1), (dict(dQ2=None, dK2=None), 1),
-    (dict(d1=96), 2), (dict(B=0), 0), (dict(NK=5_000_000, d1=256), 2),
+    (dict(d1=100), 2), (dict(B=0), 0), (dict(NK=5_000_000, d1=256), 2),
 ])
 def test_bwd_ex_argument_checks(sk, strategy, kw, expect):
     assert bwd_ex_call(sk, strategy, **kw) == expect
@@ -132,7 +132,7 @@ def test_bwd_choose_follows_the_adaptive_rule(sk):
     assert sk.bwd_choose(1, 1, 16, 65536, 64, 64, want=("dk2",)) == "separate"   # no dQ: dK kernel only
     assert sk.bwd_choose(1, 1, 16, 65536, 256, 256, want=("dq1", "dk1", "dq2", "dk2")) == "separate"
     assert sk.bwd_choose(1, 1, 16, 65536, 128, 128, want=("dq1", "dk1", "dq2", "dk2")) == "fused"
-    for bad in (dict(B=-1), dict(n_k=-5), dict(d1=96), dict(want=())):
+    for bad in (dict(B=-1), dict(n_k=-5), dict(d1=48), dict(want=())):
         a = dict(B=1, H=1, n_q=16, n_k=4096, d1=64, d2=64, causal=False, direction=0, want=("dq2", "dk2"))
         a.update(bad)
         with pytest.raises(sk.StreamKLError):
@@ -170,7 +170,7 @@ def split_call(sk, **kw):
 
 @pytest.mark.parametrize("kw,expect", [
     (dict(splits=0), 1), (dict(splits=-2), 1), (dict(ws=None), 1), (dict(ws=ctypes.c_void_p(0x100002)), 1),
-    (dict(ws_bytes=20 * 4 * 2 * 16 - 1), 1), (dict(kl=None), 1), (dict(Q1=None), 1), (dict(d2=96), 2),
+    (dict(ws_bytes=20 * 4 * 2 * 16 - 1), 1), (dict(kl=None), 1), (dict(Q1=None), 1), (dict(d2=72), 2),
     (dict(B=0), 0), (dict(NQ=0, ws=None, Q1=None, Q2=None, kl=None, lse1=None, lse2=None), 0),
 ])
 def test_split_argument_checks(sk, kw, expect):
@@ -200,7 +200,7 @@ def test_split_count_follows_the_adaptive_rule(sk):
     assert sk.split_count(1, 1, 1, 0, 128, 128) == 1
     # invalid or unsupported
     assert sk.split_count(-1, 1, 1, 1, 128, 128) == 0
-    assert sk.split_count(1, 1, 1, 1, 96, 128) == 0
+    assert sk.split_count(1, 1, 1, 1, 80, 128) == 0
 
 
 def test_split_merge_grid_limit(sk):
@@ -223,7 +223,7 @@ def noalloc_call(sk, **kw):
 
 
 @pytest.mark.parametrize("kw,expect", [
-    (dict(Q1=None), 1), (dict(kl=None), 1), (dict(splits=0), 1), (dict(causal=3), 1), (dict(d2=96), 2),
+    (dict(Q1=None), 1), (dict(kl=None), 1), (dict(splits=0), 1), (dict(causal=3), 1), (dict(d2=40), 2),
     (dict(B=0), 0), (dict(NQ=0), 0),
     # partials of 20 * W * B * H * N_Q bytes must fit the static scratch
     (dict(NQ=8192, splits=32), 4), (dict(B=1, NQ=1 << 20, splits=2), 4),
@@ -264,7 +264,7 @@ def act_bwd_call(sk, **kw):
 @pytest.mark.parametrize("call", [act_fwd_call, act_bwd_call])
 @pytest.mark.parametrize("kw,expect", [
     (dict(act=2), 1), (dict(act=-1), 1), (dict(Q1=None), 1), (dict(K2=None), 1), (dict(NQ=-1), 1),
-    (dict(s1=0.0), 1), (dict(causal=2), 1), (dict(Q2=MIS), 1), (dict(d1=96), 2), (dict(B=0), 0),
+    (dict(s1=0.0), 1), (dict(causal=2), 1), (dict(Q2=MIS), 1), (dict(d1=112), 2), (dict(B=0), 0),
 ])
 def test_activation_argument_checks(sk, call, kw, expect):
     assert call(sk, **kw) == expect
@@ -279,3 +279,18 @@ def test_activation_specific_checks(sk):
     assert act_bwd_call(sk, act=0) == 1          # kl, lse1, lse2 missing
     # sigmoid backward: no saved statistic needed, one gradient needed
     assert act_bwd_call(sk, dQ2=None, dK2=None) == 1
+
+
+def test_padded_head_dims_rules(sk):
+    """Head dims 32, 96, 160, 224 run the kernels of the next multiple of 64:
+    the split-K rule counts 128-row workgroups for them, and the adaptive
+    backward rule never picks the fused kernel (its dQ wait counts every
+    atomic of a 64-multiple head)."""
+    assert sk.bwd_choose(16, 1, 16, 65536, 128, 128) == "fused"
+    for d1, d2 in ((96, 128), (128, 32), (160, 224)):
+        assert sk.bwd_choose(16, 1, 16, 65536, d1, d2) == "separate"
+    # 16 heads of 16 rows: one 32-row workgroup each for 64-multiples, one
+    # 128-row workgroup each for padded dims: the same P_base = 16 here
+    assert sk.split_count(16, 1, 16, 65536, 96, 96) == 32
+    assert sk.split_count(1, 1, 512, 65536, 96, 96) == 128          # 4 workgroups of 128 rows
+    assert sk.split_count(1, 1, 512, 65536, 128, 128) == 256        # 2 workgroups of 256 rows

@@ -224,3 +224,86 @@ def test_invalid_arguments_raise(gpu_lib):
         gpu_lib.fwd(q1, k1, q2, k2, -1.0, 0.1)
     with pytest.raises(ValueError):
         gpu_lib.fwd(q1.float(), k1, q2, k2)
+
+
+DIMS = (32, 64, 96, 128, 160, 192, 224, 256)
+
+
+@pytest.mark.parametrize("d1", DIMS)
+@pytest.mark.parametrize("d2", DIMS)
+def test_every_head_dim_pair_multiple_of_32(gpu_lib, d1, d2):
+    """Every pair of head dims {32, 64, ..., 256}: the ones that are not a
+    multiple of 64 run the kernels of the next multiple of 64 on rows of their
+    real length (the extra columns read as zeros). Causal FWD and non-causal
+    REV alternate over the pairs; all four gradients, ragged extents."""
+    d = inputs.make("tiny", B=1, H=1, n_q=150, n_k=190, d1=d1, d2=d2, s1=d1 ** -0.5, s2=d2 ** -0.5)
+    k = DIMS.index(d1) + DIMS.index(d2)
+    run_case(gpu_lib, d, k % 2 == 0, k // 2 % 2)
+
+
+@pytest.mark.parametrize("d1,d2", [(32, 32), (96, 96), (160, 64), (224, 32)])
+def test_padded_dims_split_and_strategies(gpu_lib, d1, d2):
+    """Padded head dims through the split-K forward (decode-like shape) and the
+    backward strategy rule, which keeps them on the separate kernels; asking
+    for the fused kernel is refused."""
+    import torch
+    d = inputs.make("tiny", B=8, H=1, n_q=16, n_k=3000, d1=d1, d2=d2, s1=d1 ** -0.5, s2=d2 ** -0.5)
+    w = d["w"]
+    q1, k1, q2, k2 = upload(d)
+    W = gpu_lib.split_count(w.B, w.H, w.n_q, w.n_k, d1, d2)
+    assert W > 1
+    kl, l1, l2 = gpu_lib.fwd_split(q1, k1, q2, k2, w.s1, w.s2, True, 0, splits=W)
+    one = gpu_lib.fwd(q1, k1, q2, k2, w.s1, w.s2, True, 0)
+    g = to_gpu_f32(d["g"])
+    grads = gpu_lib.bwd(q1, k1, q2, k2, kl, l1, l2, g, w.s1, w.s2, True, 0, want=("dq2", "dk2"), strategy="auto")
+    with pytest.raises(gpu_lib.StreamKLError):
+        gpu_lib.bwd(q1, k1, q2, k2, kl, l1, l2, g, w.s1, w.s2, True, 0, want=("dq2", "dk2"), strategy="fused")
+    torch.cuda.synchronize()
+    ref = oracle.backward(d["Q1"], d["K1"], d["Q2"], d["K2"], w.s1, w.s2, True, 0, d["g"])
+    for got in (kl, one[0]):
+        check_rows("kl", got.cpu().numpy(), ref[0])
+    check_rows("lse1", l1.cpu().numpy(), ref[1])
+    check_rows("lse2", l2.cpu().numpy(), ref[2])
+    check_grad("dq2", grads[2].cpu().numpy(), ref[5])
+    check_grad("dk2", grads[3].cpu().numpy(), ref[6])
+
+
+@pytest.mark.parametrize("d1,d2", [(32, 224), (96, 160)])
+def test_padded_dims_sigmoid(gpu_lib, d1, d2):
+    """The sigmoid-score path on padded head dims, all four gradients."""
+    import torch
+    from oracle import sigmoid_oracle as so
+    d = inputs.make("tiny", B=1, H=2, n_q=140, n_k=170, d1=d1, d2=d2, s1=d1 ** -0.5, s2=d2 ** -0.5)
+    w = d["w"]
+    q1, k1, q2, k2 = upload(d)
+    g = to_gpu_f32(d["g"])
+    kl, m1, m2 = gpu_lib.fwd_act(q1, k1, q2, k2, w.s1, w.s2, True, 1, "sigmoid")
+    grads = gpu_lib.bwd(q1, k1, q2, k2, None, None, None, g, w.s1, w.s2, True, 1, want=ALL, activation="sigmoid")
+    torch.cuda.synchronize()
+    ref = so.backward(d["Q1"], d["K1"], d["Q2"], d["K2"], w.s1, w.s2, True, 1, d["g"])
+    check_rows("kl", kl.cpu().numpy(), ref[0])
+    check_rows("mass1", m1.cpu().numpy(), ref[1])
+    check_rows("mass2", m2.cpu().numpy(), ref[2])
+    for name, got, r in zip(ALL, grads, ref[3:]):
+        check_grad(name, got.cpu().numpy(), r)
+
+
+def test_padded_dims_eight_wave_grid(gpu_lib):
+    """Padded head dims with enough rows that 64-multiples would take the
+    eight-wave configuration (they take the four-wave padded one): 64 heads of
+    384 rows, d1 = 96, d2 = 32, causal, four heads against the oracle."""
+    import torch
+    d = inputs.make("tiny", B=1, H=64, n_q=384, n_k=384, d1=96, d2=32, s1=96 ** -0.5, s2=32 ** -0.5)
+    w = d["w"]
+    q1, k1, q2, k2 = upload(d)
+    g = to_gpu_f32(d["g"])
+    kl, l1, l2 = gpu_lib.fwd(q1, k1, q2, k2, w.s1, w.s2, True, 0)
+    grads = gpu_lib.bwd(q1, k1, q2, k2, kl, l1, l2, g, w.s1, w.s2, True, 0, want=ALL)
+    torch.cuda.synchronize()
+    for h in (0, 17, 63):
+        sl = lambda x: x[:, h:h + 1]  # noqa: E731
+        ref = oracle.backward(sl(d["Q1"]), sl(d["K1"]), sl(d["Q2"]), sl(d["K2"]), w.s1, w.s2, True, 0, sl(d["g"]))
+        check_rows("kl", kl[:, h:h + 1].cpu().numpy(), ref[0])
+        check_rows("lse1", l1[:, h:h + 1].cpu().numpy(), ref[1])
+        for name, got, r in zip(ALL, grads, ref[3:]):
+            check_grad(name, got[:, h:h + 1].cpu().numpy(), r)
