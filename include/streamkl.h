@@ -41,6 +41,17 @@
  *   nothing (N_K = 0 with N_Q > 0 makes every row empty). One head's rows
  *   of any tensor must span less than 4 GiB as fp32 (N * max(d1, d2) * 4 <
  *   2^32), else STREAMKL_ERR_UNSUPPORTED.
+ * - Inputs are expected finite, with every raw dot product q.k below 1e29
+ *   in magnitude (the kernels stand in -1e30 for the logit of a key a row
+ *   may not see). Non-finite values are not detected or reported. Where
+ *   they reach: the forward outputs (kl, lse1, lse2) of a query row are
+ *   non-finite if the row holds one or attends a key row that does, and
+ *   are otherwise bit for bit those of finite inputs. The backward adds a
+ *   second route: a row's masked (zero) logit gradients still multiply the
+ *   key rows of the 32-key tiles the row's block streams, so a non-finite
+ *   entry in column c of key row j can make column c of dQ non-finite for
+ *   rows of the same head that do not attend key j (0 x inf), and likewise
+ *   column c of dK from a query row. Other heads are never affected.
  * - Work is enqueued on `stream` (NULL = the default stream) and the call
  *   returns before it completes. Asynchronous faults surface at the caller's
  *   next synchronisation, as usual for HIP.

@@ -125,6 +125,29 @@ struct RowsDma {
   }
 };
 
+// The statistics of one row of a streamed tile from its saved values (valid:
+// the row exists), before the tile's fold decision; rows that do not exist
+// or have no allowed key (LSE = -inf) contribute nothing.
+__device__ __forceinline__ RowStats tile_row_stats(float la, float lb, float klv, float gv, bool valid) {
+  RowStats s{0.f, 0.f, 0.f, 0.f};
+  if (valid && la != kNegInf) {
+    s.lsa2 = la * kLog2e;
+    s.lsb2 = lb * kLog2e;
+    s.g = gv;
+    s.dl = (la - lb) + klv;
+  }
+  return s;
+}
+// ... and after it: a tile with no negative g folds |g| into the exponent
+// offsets and stores g = 1, which keeps the unfolded path exact on it.
+__device__ __forceinline__ RowStats finish_tile_row_stats(RowStats s, bool any_negative) {
+  if (!any_negative) {
+    s = fold_row_stats(s);
+    s.g = 1.f;
+  }
+  return s;
+}
+
 // Statistics of a streamed 32-row tile in LDS: [lsa2, lsb2, g, dl][row], and
 // in *fold whether g has been folded into lsa2, lsb2 (every g of the tile
 // >= 0, the usual case; the stored g is then 1): the tile loop may then skip
@@ -141,22 +164,11 @@ __device__ __forceinline__ void stage_row_stats(const float (*raw)[64], int r0, 
     return;
   }
   RowStats s{0.f, 0.f, 0.f, 0.f};
-  if (tid < BS) {
-    const float la = raw[0][tid];
-    if (r0 + tid < NQ && la != kNegInf) {   // padding and rows with no allowed key contribute nothing
-      const float lb = raw[1][tid];
-      s.lsa2 = la * kLog2e;
-      s.lsb2 = lb * kLog2e;
-      s.g = has_g ? raw[3][tid] : 1.f;
-      s.dl = (la - lb) + raw[2][tid];
-    }
-  }
+  if (tid < BS)
+    s = tile_row_stats(raw[0][tid], raw[1][tid], raw[2][tid], has_g ? raw[3][tid] : 1.f, r0 + tid < NQ);
   const bool any_negative = __builtin_amdgcn_ballot_w64(tid < BS && s.g < 0.f) != 0;
   if (tid < BS) {
-    if (!any_negative) {   // g = 1 keeps the unfolded path exact on a folded tile
-      s = fold_row_stats(s);
-      s.g = 1.f;
-    }
+    s = finish_tile_row_stats(s, any_negative);
     float* p = reinterpret_cast<float*>(&dst[0][0]);
     p[0 * BS + tid] = s.lsa2;
     p[1 * BS + tid] = s.lsb2;
@@ -165,6 +177,40 @@ __device__ __forceinline__ void stage_row_stats(const float (*raw)[64], int r0, 
     if (tid == 0) *fold = any_negative ? 0 : 1;
   }
 }
+
+// ----------------------------------------------------------------------------
+// Row statistics prepared ahead of the dK kernel. In the dK kernel the 32
+// streamed rows of a tile lie along the registers of every lane, so their
+// statistics pass through LDS; formed in the tile loop, one wave per tile
+// does that work (stage_row_stats) while the other waves wait for it at the
+// tile's barrier. kl_bwd_rowstats_kernel forms them for every tile of every
+// head beforehand, with the same arithmetic bit for bit: tile T = head * ntq
+// + t (ntq = ceil(N_Q / 32)) as stats[T][4][32] floats (lsa2, lsb2, g, dl by
+// row) and fold[T], whether the tile's g are folded (the kernel is in
+// kl_bwd_rowstats.hip). The dK kernel then streams each tile's 512 bytes and
+// flag into LDS with its query tile.
+// ----------------------------------------------------------------------------
+constexpr int kRowStatsTile = 32;
+constexpr int kRowStatsTilesPerBlock = 8;
+
+// Direct-to-LDS loads of one prepared tile (512 bytes: two dword loads of the
+// wave) and its fold flag (one lane), issued by one wave.
+struct PreparedStatsDma {
+  rsrc_t r_s, r_f;
+  __device__ __forceinline__ PreparedStatsDma(const float* stats, const int* fold, size_t head_tile0, int ntq) {
+    const bool on = stats != nullptr;
+    r_s = make_rsrc(on ? stats + head_tile0 * 4 * kRowStatsTile : stats, on ? (uint32_t)ntq * 512u : 0u);
+    r_f = make_rsrc(on ? fold + head_tile0 : fold, on ? (uint32_t)ntq * 4u : 0u);
+  }
+  __device__ __forceinline__ void issue(int t, float* dst, int* fold_dst, int lane) const {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const uint32_t off = (uint32_t)t * 512u + (uint32_t)lane * 4u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r_s, (lds_void*)dst, 4, off, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r_s, (lds_void*)(dst + 64), 4, off + 256u, 0, 0, 0);
+    if (lane == 0) __builtin_amdgcn_raw_ptr_buffer_load_lds(r_f, (lds_void*)fold_dst, 4, (uint32_t)t * 4u, 0, 0, 0);
+#endif
+  }
+};
 
 // Logit gradients of one element (raw dot products ra, rb). FOLD: the row's
 // |g| is already folded into the exponent offsets (lsa2, lsb2 lowered by
@@ -190,7 +236,9 @@ __device__ __forceinline__ void dlogits(float ra, float rb, bool ok, float ca, f
   }
   if constexpr (WANT_A) {
     const float u = __builtin_fmaf(ra, sa, -__builtin_fmaf(rb, sb, s.dl));
-    dsa = FOLD ? pa * u : (s.g * pa) * u;
+    // p = 0 on a masked entry; select 0 rather than multiply, so that a
+    // non-finite logit of a key the row may not see stays out of its row
+    dsa = ok ? (FOLD ? pa * u : (s.g * pa) * u) : 0.f;
   }
 }
 
@@ -402,10 +450,9 @@ kl_bwd_dq_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   // the wave index is uniform: in a scalar register, so are the values derived from it
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), half = lane >> 5;
   const int TQ = (NQ + C::BR - 1) / C::BR;
-  const int logical = xcd_logical(blockIdx.x, gridDim.x);
-  const int bh = logical / TQ;
-  int qt = logical - bh * TQ;
-  if (CAUSAL) qt = TQ - 1 - qt;
+  int bh, qt;
+  head_block<CAUSAL, C::MINB>(TQ, bh, qt);
+  if (CAUSAL) qt = TQ - 1 - qt;   // rank 0: the last rows, the longest
   const int q0 = qt * C::BR;
   const int off = NK - NQ;
   const int qw = q0 + 32 * wave;
@@ -505,7 +552,8 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
                  int NQ, int NK, int dra, int drb, float sa, float sb,
                  const float* __restrict__ kl, const float* __restrict__ lse_a,
                  const float* __restrict__ lse_b, const float* __restrict__ g,
-                 float* __restrict__ dKa, float* __restrict__ dKb) {
+                 float* __restrict__ dKa, float* __restrict__ dKb,
+                 const float* __restrict__ pstats, const int* __restrict__ pfold) {
   // PD: the head dims may be padded (the rows in memory are dra, drb long);
   // otherwise they are the compile-time ones and the runtime values unused
   if constexpr (!PD) {
@@ -525,9 +573,9 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   // the wave index is uniform: in a scalar register, so are the values derived from it
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6), half = lane >> 5;
   const int TK = (NK + C::BR - 1) / C::BR;
-  const int logical = xcd_logical(blockIdx.x, gridDim.x);
-  const int bh = logical / TK;
-  const int kb0 = (logical - bh * TK) * C::BR;   // causal: low key blocks see the most rows, so they go first
+  int bh, kblk;
+  head_block<CAUSAL, C::MINB>(TK, bh, kblk);   // causal rank 0: the first keys, seen by the most rows
+  const int kb0 = kblk * C::BR;
   const int off = NK - NQ;
   const int kw = kb0 + 32 * wave;
   const int myk = kw + (lane & 31);
@@ -559,6 +607,10 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
   const TileDma<C::BS, C::CA, C::CB> dma(tid, dra / 8, drb / 8);
 
   const RowsDma rdma(kl, lse_a, lse_b, g, (size_t)bh * NQ, NQ);
+  // prepared statistics (kl_bwd_rowstats_kernel), when the caller made them
+  static_assert(C::BS == kRowStatsTile, "prepared statistics come in tiles of the streamed rows");
+  const bool pre = ACT == kActSoftmax && pstats != nullptr;
+  const PreparedStatsDma pdma(pre ? pstats : nullptr, pfold, (size_t)bh * ntq, ntq);
 
   const TrOffsets<DA, DB, MODE> tro(lane);
   auto tile = [&](const u32x4* stage, int buf, int t) {
@@ -595,27 +647,38 @@ kl_bwd_dk_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ K
     }
   };
 
-  // The row values of tile t + 1 are turned into statistics by wave 0 early
-  // in step t, while the tile is computed: they were loaded with the
-  // previous tile, so no wait sits between the end-of-step wait and barrier.
+  // Without prepared statistics, the row values of tile t + 1 are turned
+  // into statistics by wave 0 early in step t, while the tile is computed:
+  // they were loaded with the previous tile, so no wait sits between the
+  // end-of-step wait and barrier. With them, wave 0 streams tile t + 1's
+  // statistics and flag straight into their stage during step t.
   auto stats_in = [&](int t, float (*raw)[64], int buf) {
     if (wave == 0) stage_row_stats<C::BS, ACT>(raw, t * C::BS, NQ, rdma.has_g, sstat[buf], &sfold[buf], tid);
   };
+  auto pre_in = [&](int t, int buf) {
+    if (wave == 0) pdma.issue(t, reinterpret_cast<float*>(&sstat[buf][0][0]), &sfold[buf], lane);
+  };
   if (t_begin < ntq) {
     dma.issue(rqa, rqb, t_begin * C::BS, st0, wave, dra, drb);
-    if (wave == 0) {
+    if (pre) {
+      pre_in(t_begin, 0);
+    } else if (wave == 0) {
       rdma.issue<ACT>(t_begin * C::BS, sraw0, lane);
       if (t_begin + 1 < ntq) rdma.issue<ACT>((t_begin + 1) * C::BS, sraw1, lane);
     }
     wait_vmem();
-    stats_in(t_begin, sraw0, 0);
+    if (!pre) stats_in(t_begin, sraw0, 0);
   }
   __syncthreads();
   // rnext holds the row values of tile t + 1; rfree receives those of t + 2
   auto step = [&](const u32x4* cur, u32x4* nxt, float (*rnext)[64], float (*rfree)[64], int t, int buf) {
     if (t + 1 < ntq) dma.issue(rqa, rqb, (t + 1) * C::BS, nxt, wave, dra, drb);
-    if (wave == 0 && t + 2 < ntq) rdma.issue<ACT>((t + 2) * C::BS, rfree, lane);
-    if (t + 1 < ntq) stats_in(t + 1, rnext, buf ^ 1);
+    if (pre) {
+      if (t + 1 < ntq) pre_in(t + 1, buf ^ 1);
+    } else {
+      if (wave == 0 && t + 2 < ntq) rdma.issue<ACT>((t + 2) * C::BS, rfree, lane);
+      if (t + 1 < ntq) stats_in(t + 1, rnext, buf ^ 1);
+    }
     tile(cur, buf, t);
     wait_vmem();
     __syncthreads();

@@ -128,10 +128,13 @@ __device__ __forceinline__ f32x16 dq_block_mma(const u32x4* ds_tile, const u32x4
   return acc;
 }
 
-// One atomic add per element of the 32 x 32 dQ tile (16 per lane). When every
-// row of the tile exists and sees the key block (FULL), all 16 are issued
-// unconditionally, so the number of vector memory instructions is known;
-// otherwise lanes without a row are masked off.
+// One atomic add per element of the 32 x 32 dQ tile (kDqAtomicsPerBlock per
+// lane). When every row of the tile exists and sees the key block (FULL),
+// all of them are issued unconditionally, in straight-line code, so the
+// number of vector memory instructions is known (the end-of-tile wait relies
+// on it); otherwise lanes without a row are masked off.
+constexpr int kDqAtomicsPerBlock = 16;
+static_assert(sizeof(f32x16) / sizeof(float) == kDqAtomicsPerBlock, "one atomic per accumulator register");
 template <int D, bool CAUSAL, bool FULL>
 __device__ __forceinline__ void dq_block_add(const f32x16& acc, int cb, int lane, float* __restrict__ dq,
                                              size_t row_base, int q0, int NQ, int qmin_seen, float s) {
@@ -139,7 +142,7 @@ __device__ __forceinline__ void dq_block_add(const f32x16& acc, int cb, int lane
   const int qh = q0 + 4 * half;   // row of register 0; register i adds 8 (i / 4) + i % 4
   float* out = dq + (row_base + qh) * D + 32 * cb + (lane & 31);
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
+  for (int i = 0; i < kDqAtomicsPerBlock; ++i) {
     const int ri = 8 * (i >> 2) + (i & 3);
     const int q = qh + ri;
     if (FULL || (q < NQ && (!CAUSAL || q >= qmin_seen))) atomic_add_global(out + ri * D, acc[i] * s);
@@ -291,8 +294,9 @@ kl_bwd_fused_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict_
     }
   };
   // Returns how many of this wave's last vector memory instructions are
-  // atomics that the next wait may leave in flight: 16 per item of a full
-  // tile, 0 when the tile is partial (some adds masked off, count unknown).
+  // atomics that the next wait may leave in flight: kDqAtomicsPerBlock per
+  // item of a full tile, 0 when the tile is partial (some adds masked off,
+  // count unknown).
   auto dq_add = [&](const DqWork& w) {
     const int qmin_seen = kb0 - off;   // earlier rows see no key of the block
     const bool full = w.r0 + C::BS <= NQ && (!CAUSAL || w.r0 >= qmin_seen);
@@ -307,7 +311,7 @@ kl_bwd_fused_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict_
               dq_block_add<DB, CAUSAL, true>(w.acc[m], it, lane, dQb, (size_t)bh * NQ, w.r0, NQ, qmin_seen, sb);
             else
               dq_block_add<DB, CAUSAL, false>(w.acc[m], it, lane, dQb, (size_t)bh * NQ, w.r0, NQ, qmin_seen, sb);
-            issued += 16;
+            issued += kDqAtomicsPerBlock;
           }
         } else if constexpr (C::WANT_A) {
           if (dQa) {
@@ -317,7 +321,7 @@ kl_bwd_fused_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict_
             else
               dq_block_add<DA, CAUSAL, false>(w.acc[m], it - C::NCB_B, lane, dQa, (size_t)bh * NQ, w.r0, NQ,
                                               qmin_seen, sa);
-            issued += 16;
+            issued += kDqAtomicsPerBlock;
           }
         }
       }
@@ -337,7 +341,14 @@ kl_bwd_fused_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict_
     DqWork w;
     if (prev >= 0) dq_compute(prev, w);
     if (has_next) stage_in(tile_at(i + 1), nxt);
+    // The end-of-tile wait below leaves the newest kDqAtomicsPerBlock vector
+    // memory instructions in flight. That is safe only because every one of
+    // them is an atomic issued after the last load of the next tile: vector
+    // memory instructions complete in issue order, so all loads are done.
+    // Nothing may move between the loads and the atomics.
+    __builtin_amdgcn_sched_barrier(0);
     const int n_atomic = prev >= 0 ? dq_add(w) : 0;
+    __builtin_amdgcn_sched_barrier(0);
 
     const int r0 = t * C::BS;
     const int qlast = min(r0 + C::BS, NQ) - 1;
@@ -376,9 +387,10 @@ kl_bwd_fused_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict_
     if constexpr (C::WANT_B) store_ds(ds_b, kloc, half, dsb);
     if (active) bwd_grad_tile<DA, DB, MODE>(cur, dsa, dsb, dka, dkb, tro);
     if (has_next) {
-      // vector memory operations complete in issue order: with the last 16
-      // (atomics) allowed in flight, the next tile's loads are done
-      if (n_atomic >= 16) wait_vmem_le<16>();
+      // vector memory operations complete in issue order: with the newest
+      // kDqAtomicsPerBlock (atomics, see above) allowed in flight, the next
+      // tile's loads are done
+      if (n_atomic >= kDqAtomicsPerBlock) wait_vmem_le<kDqAtomicsPerBlock>();
       else wait_vmem();
       stage_row_stats<C::BS>(raw_of(nxt), tile_at(i + 1) * C::BS, NQ, rdma.has_g, sstat[buf ^ 1], &sfold[buf ^ 1],
                              tid);

@@ -26,7 +26,7 @@ hipError_t run_bwd_dk(const BwdArgs& a) {
   const dim3 grid((unsigned)((long long)a.BH * tiles));
   hipLaunchKernelGGL((kl_bwd_dk_kernel<DA, DB, CAUSAL, MODE, ACT, PD>), grid, dim3(kThreads), 0, a.stream,
                      a.Qa, a.Ka, a.Qb, a.Kb, a.NQ, a.NK, a.dra, a.drb, a.sa, a.sb, a.kl, a.lse_a, a.lse_b, a.g,
-                     a.dKa, a.dKb);
+                     a.dKa, a.dKb, a.pstats, a.pfold);
   return hipGetLastError();
 }
 

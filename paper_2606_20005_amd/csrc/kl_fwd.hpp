@@ -511,10 +511,9 @@ kl_fwd_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
   __shared__ u32x4 st1[C::STAGE];
   __shared__ float tot[SoftmaxRows::NTOT * C::NT];
   const int TQ = (NQ + C::BQ - 1) / C::BQ;
-  const int logical = xcd_logical(blockIdx.x, gridDim.x);
-  const int bh = logical / TQ;
-  int qt = logical - bh * TQ;
-  if (CAUSAL) qt = TQ - 1 - qt;   // longest rows first
+  int bh, qt;
+  head_block<CAUSAL, C::MINB>(TQ, bh, qt);
+  if (CAUSAL) qt = TQ - 1 - qt;   // rank 0: the last rows, the longest
   int myq;
   const RowPartial p =
       fwd_pass<C, CAUSAL>(st0, st1, tot, Qa, Ka, Qb, Kb, NQ, NK, dra, drb, ca, cb, bh, qt * C::BQ, 0, 1 << 30,
@@ -540,10 +539,9 @@ kl_fwd_sigmoid_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restric
   __shared__ u32x4 st1[C::STAGE];
   __shared__ float tot[SigmoidRows::NTOT * C::NT];
   const int TQ = (NQ + C::BQ - 1) / C::BQ;
-  const int logical = xcd_logical(blockIdx.x, gridDim.x);
-  const int bh = logical / TQ;
-  int qt = logical - bh * TQ;
-  if (CAUSAL) qt = TQ - 1 - qt;   // longest rows first
+  int bh, qt;
+  head_block<CAUSAL, C::MINB>(TQ, bh, qt);
+  if (CAUSAL) qt = TQ - 1 - qt;   // rank 0: the last rows, the longest
   int myq;
   const SigmoidPartial p = fwd_pass<C, CAUSAL, SigmoidRows>(st0, st1, tot, Qa, Ka, Qb, Kb, NQ, NK, dra, drb, ca, cb,
                                                             bh, qt * C::BQ, 0, 1 << 30, myq);

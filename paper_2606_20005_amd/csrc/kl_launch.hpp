@@ -31,6 +31,9 @@ struct BwdArgs {
   float *dQa, *dQb, *dKa, *dKb;
   int act;                      // 0: softmax scores; 1: sigmoid scores (kl and the LSEs unused)
   hipStream_t stream;
+  // row statistics prepared by launch_bwd_rowstats for the dK kernel (null: it forms them itself)
+  const float* pstats = nullptr;
+  const int* pfold = nullptr;
 };
 
 // Each returns hipErrorInvalidValue for a head-dim pair it does not hold,
@@ -48,6 +51,12 @@ int fwd_rows_per_workgroup(int da, int db, int n_q, long long bh, bool causal, b
 int fwd_merge_rows_per_workgroup();
 hipError_t launch_bwd_dq(int da, int db, bool causal, int mode, const BwdArgs& a);
 hipError_t launch_bwd_dk(int da, int db, bool causal, int mode, const BwdArgs& a);
+// Floats of the prepared row statistics of the dK kernel (kl_bwd_rowstats_kernel):
+// 128 per 32-row tile plus one int flag per tile.
+size_t bwd_rowstats_floats(int bh, int nq);
+// Prepares them into stats (the flags follow the 128-float tiles) and points
+// a.pstats, a.pfold at them; softmax scores only.
+hipError_t launch_bwd_rowstats(BwdArgs& a, float* stats);
 hipError_t launch_bwd_dq_m1(int da, int db, bool causal, const BwdArgs& a);
 hipError_t launch_bwd_dq_m2(int da, int db, bool causal, const BwdArgs& a);
 hipError_t launch_bwd_dq_m3(int da, int db, bool causal, const BwdArgs& a);

@@ -330,6 +330,23 @@ int bwd_common(const void* Q1, const void* K1, const void* Q2, const void* K2, i
     if (e == hipSuccess) e = streamkl::launch_bwd_fused(kda, kdb, causal == 1, m.q | m.k, a);
     return hip_status(e);
   }
+  // With a dQ output and softmax scores, the dK kernel's row statistics are
+  // prepared ahead (kl_bwd_rowstats_kernel) into that dQ output, which the
+  // dQ kernel overwrites afterwards: dK then runs first. The stream orders
+  // the three launches; the caller sees only the final dQ.
+  float* scratch = nullptr;
+  if (m.k && m.q && !sig) {
+    float* dq = a.dQb ? a.dQb : a.dQa;
+    const size_t room = (size_t)bh * N_Q * (a.dQb ? db : da);
+    if (streamkl::bwd_rowstats_floats(a.BH, N_Q) <= room) scratch = dq;
+  }
+  if (scratch) {
+    BwdArgs ak = a;
+    e = streamkl::launch_bwd_rowstats(ak, scratch);
+    if (e == hipSuccess) e = streamkl::launch_bwd_dk(kda, kdb, causal == 1, m.k, ak);
+    if (e == hipSuccess) e = streamkl::launch_bwd_dq(kda, kdb, causal == 1, m.q, a);
+    return hip_status(e);
+  }
   if (m.q) e = streamkl::launch_bwd_dq(kda, kdb, causal == 1, m.q, a);
   if (e == hipSuccess && m.k && N_K > 0) e = streamkl::launch_bwd_dk(kda, kdb, causal == 1, m.k, a);
   return hip_status(e);

@@ -117,6 +117,39 @@ def test_upstream_gradient_signs(gpu_lib, pattern, strategy):
         run_case(gpu_lib, d, causal, 0, strategy=strategy)
 
 
+@pytest.mark.parametrize("pattern", ["ones", "none", "mixed", "some_tiles", "magnitudes"])
+@pytest.mark.parametrize("n_q,n_k,d1,d2,causal,direction", [
+    (200, 700, 64, 64, True, 0), (1000, 300, 128, 64, False, 1), (33, 129, 64, 128, True, 0),
+    (3, 300, 32, 32, False, 0), (257, 257, 96, 160, True, 1),
+])
+def test_dk_prepared_statistics_match_in_kernel_staging(gpu_lib, pattern, n_q, n_k, d1, d2, causal, direction):
+    """When a dQ is requested too, the dK kernel streams row statistics that a
+    prep kernel wrote into that dQ output beforehand; alone, it forms them
+    itself. Same arithmetic: dK bit for bit equal either way, for every g
+    pattern (folded and unfolded tiles, g absent), ragged tails, both
+    directions, padded dims and a dQ too small to hold them (3 rows of d = 32:
+    in-kernel path on both sides). The dQ written over the prepared values
+    equals a dQ-only call bit for bit."""
+    import torch
+    d = inputs.make("tiny", B=1, H=2, n_q=n_q, n_k=n_k, d1=d1, d2=d2, s1=d1 ** -0.5, s2=d2 ** -0.5)
+    w = d["w"]
+    q1, k1, q2, k2 = upload(d)
+    g = None if pattern == "none" else to_gpu_f32(np.ones_like(d["g"]) if pattern == "ones"
+                                                   else _signed_g(d["g"].shape, pattern))
+    kl, l1, l2 = gpu_lib.fwd(q1, k1, q2, k2, w.s1, w.s2, causal, direction)
+    args = (q1, k1, q2, k2, kl, l1, l2, g, w.s1, w.s2, causal, direction)
+    for pair in (("dq2", "dk2"), ("dq1", "dk1"), ALL):
+        both = gpu_lib.bwd(*args, want=pair)
+        dk_only = gpu_lib.bwd(*args, want=tuple(n for n in pair if n.startswith("dk")))
+        dq_only = gpu_lib.bwd(*args, want=tuple(n for n in pair if n.startswith("dq")))
+        torch.cuda.synchronize()
+        for x, y, z in zip(both, dk_only, dq_only):
+            if x is None:
+                continue
+            ref = y if y is not None else z
+            assert torch.equal(x, ref), pair
+
+
 @pytest.mark.parametrize("name,over,causal", [
     ("distill", dict(H=2, n_q=512, n_k=512), True),
     ("mid", dict(H=2, n_q=512, n_k=512), False),
@@ -307,3 +340,44 @@ def test_padded_dims_eight_wave_grid(gpu_lib):
         check_rows("lse1", l1[:, h:h + 1].cpu().numpy(), ref[1])
         for name, got, r in zip(ALL, grads, ref[3:]):
             check_grad(name, got[:, h:h + 1].cpu().numpy(), r)
+
+
+@pytest.mark.parametrize("where", ["query", "key"])
+def test_nonfinite_inputs_stay_in_the_rows_that_see_them(gpu_lib, where):
+    """The documented reach of a non-finite input. An infinity in query row 7
+    of head 0 (or in column 5 of key row 20, causal, so that rows 0-19 never
+    attend it): the forward outputs of the rows that do not see it are bit
+    for bit those of finite inputs; their dQ rows too, except, for the key
+    case, column 5 of dQ1 (a masked zero weight times the key row of the
+    same tile); head 1 is untouched in every output, dK included."""
+    import torch
+    n = 120
+    d = inputs.make("tiny", B=1, H=2, n_q=n, n_k=n)
+    w = d["w"]
+    clean = upload(d)
+    bad_np = {k: d[k].copy() for k in ("Q1", "K1", "Q2", "K2")}
+    cols = np.ones(d["Q1"].shape[-1], dtype=bool)
+    if where == "query":
+        bad_np["Q1"][0, 0, 7, 3] = np.inf
+        causal, affected = False, np.zeros(n, dtype=bool)
+        affected[7] = True
+    else:
+        bad_np["K1"][0, 0, 20, 5] = np.inf
+        causal, affected = True, np.arange(n) >= 20
+        cols[5] = False
+    bad = upload(bad_np)
+    outs = []
+    for q1, k1, q2, k2 in (clean, bad):
+        kl, l1, l2 = gpu_lib.fwd(q1, k1, q2, k2, w.s1, w.s2, causal, 0)
+        grads = gpu_lib.bwd(q1, k1, q2, k2, kl, l1, l2, None, w.s1, w.s2, causal, 0, want=ALL)
+        torch.cuda.synchronize()
+        outs.append([t.cpu().numpy() for t in (kl, l1, l2, *grads)])
+    (kl0, a0, b0, q10, k10, q20, k20), (kl1, a1, b1, q11, k11, q21, k21) = outs
+    for x, y in zip(outs[0], outs[1]):   # head 1
+        assert np.array_equal(x[0, 1], y[0, 1])
+    keep = ~affected
+    for x, y in ((kl0, kl1), (a0, a1), (b0, b1), (q20, q21)):
+        assert np.array_equal(x[0, 0, keep], y[0, 0, keep])
+    assert np.array_equal(q10[0, 0, keep][:, cols], q11[0, 0, keep][:, cols])
+    assert not np.isfinite(kl1[0, 0, affected]).any()
+    assert not np.isfinite(q11[0, 0, affected]).all(axis=-1).any()
