@@ -226,8 +226,11 @@ extern "C" int streamkl_fwd_split_count(int B, int H, int N_Q, int N_K, int d1, 
   constexpr long long kTarget = 512;   // two workgroups per CU on 256 CUs
   const int bq = streamkl::fwd_rows_per_workgroup(kernel_dim(d1), kernel_dim(d2), N_Q, (long long)B * H, false,
                                                   d1 % 64 != 0 || d2 % 64 != 0);
-  const long long base = (long long)B * H * ((N_Q + bq - 1) / bq);
-  if (base == 0 || base >= kTarget) return 1;
+  // base = B*H * query blocks, compared with the target without forming a
+  // product that could overflow
+  const long long bh = (long long)B * H, qb = ((long long)N_Q + bq - 1) / bq;
+  if (bh == 0 || qb == 0 || bh >= kTarget || qb >= kTarget || bh * qb >= kTarget) return 1;
+  const long long base = bh * qb;
   const long long tiles = (N_K + 31LL) / 32;
   const long long w = kTarget / base < tiles ? kTarget / base : tiles;
   return w < 1 ? 1 : (int)w;
