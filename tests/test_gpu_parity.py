@@ -162,6 +162,17 @@ def test_workload_structures_reduced(gpu_lib, name, over, causal):
     run_case(gpu_lib, inputs.make(name, **over), causal, 0)
 
 
+@pytest.mark.parametrize("H,n,d1,d2", [(8, 640, 128, 64), (16, 333, 64, 64), (24, 300, 128, 128)])
+def test_causal_rank_order_grids(gpu_lib, H, n, d1, d2):
+    """Causal grids whose heads split evenly over the 8 XCDs and that fit in a
+    few rounds of resident workgroups are handed out rank by rank per XCD (1,
+    2 and 3 heads per XCD here, ragged row counts): every row and key of every
+    head against the oracle, all four gradients, both directions."""
+    d = inputs.make("distill", B=1, H=H, n_q=n, n_k=n, d1=d1, d2=d2, s1=d1 ** -0.5, s2=d2 ** -0.5)
+    run_case(gpu_lib, d, True, 0)
+    run_case(gpu_lib, d, True, 1, want=("dq1", "dk1", "dq2", "dk2"))
+
+
 def test_causal_eight_wave_forward_reduced(gpu_lib):
     """1024 heads of 256 rows: B*H*ceil(N_Q/256) = 1024 workgroups, enough that
     the causal forward takes its eight-wave, 256-row configuration (the one the
