@@ -410,8 +410,9 @@ def sigmoid_figures(sk, evict, reps=10):
     drawn on the device), non-causal and causal: forward, dQ2 and dK2 kernels,
     median of `reps` event-timed calls each after a cache-evicting write.
     TFLOP/s count the same MFMA work as the softmax path; the kernels
-    themselves are bound by vector and transcendental issue (three
-    transcendental instructions per score and distribution)."""
+    themselves are bound by vector and transcendental issue (per score
+    pair: two v_exp_f32 and two v_rcp_f32, and one v_log_f32 where the
+    log-ratio is needed)."""
     import torch
     B, H, N, D = 1, 32, 16384, 128
     gen = torch.Generator(device="cuda")

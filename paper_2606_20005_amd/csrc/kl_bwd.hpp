@@ -220,11 +220,16 @@ template <bool WANT_A, bool WANT_B, bool FOLD = false, int ACT = kActSoftmax>
 __device__ __forceinline__ void dlogits(float ra, float rb, bool ok, float ca, float cb, float sa, float sb,
                                         const RowStats& s, float& dsa, float& dsb) {
   if constexpr (ACT == kActSigmoid) {
-    // ca, cb = s * log2(e): sigmoid_terms takes the logit in base-2 units;
-    // nl_b - nl_a = log2 A_a - log2 A_b
-    const SigmoidTerms ta = sigmoid_terms(ra * ca), tb = sigmoid_terms(rb * cb);
-    if constexpr (WANT_B) dsb = ok ? s.g * ((tb.a - ta.a) * tb.na) : 0.f;
-    if constexpr (WANT_A) dsa = ok ? s.g * (ta.a * ta.na) * ((tb.nl - ta.nl) * kLn2) : 0.f;
+    // ca, cb = s * log2(e): the helpers take the logits in base-2 units;
+    // lr = log2 A_a - log2 A_b, needed for dS_a only
+    if constexpr (WANT_A) {
+      const SigmoidPair t = sigmoid_pair(ra * ca, rb * cb);
+      if constexpr (WANT_B) dsb = ok ? s.g * ((t.b - t.a) * t.nb) : 0.f;
+      dsa = ok ? s.g * (t.a * t.na) * (t.lr * kLn2) : 0.f;
+    } else {
+      const SigmoidTerms ta = sigmoid_terms(ra * ca), tb = sigmoid_terms(rb * cb);
+      dsb = ok ? s.g * ((tb.a - ta.a) * tb.na) : 0.f;
+    }
     return;
   }
   const float xa = ok ? __builtin_fmaf(ra, ca, -s.lsa2) : kNegInf;

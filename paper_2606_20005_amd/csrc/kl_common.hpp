@@ -38,21 +38,44 @@ __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const
 // 2^x on the transcendental unit (v_exp_f32); exp2(-inf) = 0.
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// What the sigmoid-score divergence needs of one scaled logit z = S log2(e):
-// a = sigmoid(S), na = 1 - a = sigmoid(-S) and nl = -log2 sigmoid(S) =
-// max(-z, 0) + log2(1 + 2^-|z|), formed from e = 2^-|z| in (0, 1] so that
-// nothing overflows and 1 - a is not a cancellation. A masked stand-in
-// logit (-1e30) gives a = 0, na = 1 and a finite nl.
+// What the sigmoid-score divergence needs of the two scaled logits za, zb
+// (z = S log2(e)) of one (row, key) pair: A = sigmoid(S), 1 - A = sigmoid(-S)
+// for both, and lr = log2(A_a / A_b). With e = 2^-|z| in (0, 1] and
+// w = 1 + e, A = 1/w or e/w and -log2 A = max(-z, 0) + log2 w, so
+//   lr = max(-zb, 0) - max(-za, 0) + log2(w_b / w_a),
+//   w_b / w_a = 1 + (e_b - e_a) / w_a:
+// one log2, with the reciprocal 1/w_a already formed for A_a, where the two
+// logarithms taken separately would cost a second transcendental; written
+// as 1 + (e_b - e_a)/w_a the ratio is exactly 1 for equal logits, so equal
+// score rows give lr = 0 exactly. Nothing overflows and 1 - A is no
+// cancellation. A masked stand-in logit (-1e30) gives A = 0, 1 - A = 1 and a
+// finite lr.
+// The terms of one logit alone, for gradients that need no logarithm:
+// a = sigmoid(S), na = 1 - a.
 struct SigmoidTerms {
-  float a, na, nl;
+  float a, na;
 };
 __device__ __forceinline__ SigmoidTerms sigmoid_terms(float z) {
   const float e = __builtin_amdgcn_exp2f(-fabsf(z));
-  const float w = 1.f + e;                          // in (1, 2]
-  const float iw = __builtin_amdgcn_rcpf(w);
+  const float iw = __builtin_amdgcn_rcpf(1.f + e);
   const float ew = e * iw;
   const bool pos = z >= 0.f;
-  return SigmoidTerms{pos ? iw : ew, pos ? ew : iw, fmaxf(-z, 0.f) + __builtin_amdgcn_logf(w)};
+  return SigmoidTerms{pos ? iw : ew, pos ? ew : iw};
+}
+
+struct SigmoidPair {
+  float a, na;   // A_a, 1 - A_a
+  float b, nb;   // A_b, 1 - A_b
+  float lr;      // log2(A_a / A_b)
+};
+__device__ __forceinline__ SigmoidPair sigmoid_pair(float za, float zb) {
+  const float ea = __builtin_amdgcn_exp2f(-fabsf(za)), eb = __builtin_amdgcn_exp2f(-fabsf(zb));
+  const float wa = 1.f + ea, wb = 1.f + eb;   // in (1, 2]
+  const float iwa = __builtin_amdgcn_rcpf(wa), iwb = __builtin_amdgcn_rcpf(wb);
+  const float ewa = ea * iwa, ewb = eb * iwb;
+  const bool pa = za >= 0.f, pb = zb >= 0.f;
+  const float lr = (fmaxf(-zb, 0.f) - fmaxf(-za, 0.f)) + __builtin_amdgcn_logf(__builtin_fmaf(eb - ea, iwa, 1.f));
+  return SigmoidPair{pa ? iwa : ewa, pa ? ewa : iwa, pb ? iwb : ewb, pb ? ewb : iwb, lr};
 }
 
 __device__ __forceinline__ f32x16 zero16() {

@@ -298,11 +298,11 @@ struct SoftmaxRows {
 // Sigmoid scores (Sec. 3.1, "Generalizability beyond Softmax"): A_t =
 // sigmoid(S_t) with no normalisation, and the row value is the generalized
 // KL sum_j [A_a log(A_a / A_b) - A_a + A_b] over the visible keys. With
-// nl = -log2 A (sigmoid_terms) a lane keeps four plain sums over its keys:
-// acc = sum A_a (nl_b - nl_a) (base 2), dif = sum (A_b - A_a) and the masses
+// lr = log2(A_a / A_b) (sigmoid_pair) a lane keeps four plain sums over its
+// keys: acc = sum A_a lr (base 2), dif = sum (A_b - A_a) and the masses
 // sum A_a, sum A_b; L = acc ln 2 + dif. No maximum or rescaling is needed:
-// every term is bounded (A <= 1, |nl| <= |z| + 1). Chunk totals and the two
-// half-waves combine by addition.
+// every term is bounded (A <= 1, |lr| <= |za| + |zb| + 1). Chunk totals and
+// the two half-waves combine by addition.
 struct SigmoidPartial {
   float acc, dif, ma, mb;
 };
@@ -317,12 +317,12 @@ struct SigmoidRows {
     float acc[2] = {0.f, 0.f}, dif[2] = {0.f, 0.f}, ma[2] = {0.f, 0.f}, mb[2] = {0.f, 0.f};
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const SigmoidTerms ta = sigmoid_terms(sa[i] * ca), tb = sigmoid_terms(sb[i] * cb);
+      const SigmoidPair t = sigmoid_pair(sa[i] * ca, sb[i] * cb);
       const int k = i & 1;
-      acc[k] = __builtin_fmaf(ta.a, tb.nl - ta.nl, acc[k]);
-      dif[k] += tb.a - ta.a;
-      ma[k] += ta.a;
-      mb[k] += tb.a;
+      acc[k] = __builtin_fmaf(t.a, t.lr, acc[k]);
+      dif[k] += t.b - t.a;
+      ma[k] += t.a;
+      mb[k] += t.b;
     }
     s.acc += acc[0] + acc[1];
     s.dif += dif[0] + dif[1];
