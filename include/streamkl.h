@@ -131,6 +131,11 @@ int streamkl_fwd(const void* Q1, const void* K1, const void* Q2, const void* K2,
  * dkl: per-row upstream gradient g; NULL means g = 1 for every row.
  * dQ1, dK1, dQ2, dK2: each NULL (not computed) or written in full
  * (overwritten, never accumulated into). At least one must be non-NULL.
+ * The outputs must not overlap each other or the inputs. When a dK and a dQ
+ * are both requested, the call first writes the dK kernel's per-row
+ * statistics into one of the dQ outputs, which the dQ kernel then
+ * overwrites: work ordered after the call on `stream` sees only the final
+ * dQ, but other streams must not read a dQ output before the call completes.
  * dQ tiles are owned by query blocks and dK tiles by key blocks, so no
  * atomics are used and results are bitwise reproducible run to run (the
  * separate-kernel strategy of Sec. 4.2; streamkl_bwd_ex offers the fused one).
