@@ -139,6 +139,10 @@ int streamkl_fwd(const void* Q1, const void* K1, const void* Q2, const void* K2,
  * dQ tiles are owned by query blocks and dK tiles by key blocks, so no
  * atomics are used and results are bitwise reproducible run to run (the
  * separate-kernel strategy of Sec. 4.2; streamkl_bwd_ex offers the fused one).
+ * Both gradient pairs of a call are formed by one set of kernels while
+ * d1 + d2 < 448 (head dims rounded up to multiples of 64); from there on by
+ * the second-slot kernels followed by the first-slot ones, each recomputing
+ * the logits (one kernel holding both pairs would not fit the registers).
  */
 int streamkl_bwd(const void* Q1, const void* K1, const void* Q2, const void* K2,
                  int B, int H, int N_Q, int N_K, int d1, int d2,

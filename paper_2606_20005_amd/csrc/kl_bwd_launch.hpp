@@ -44,10 +44,14 @@ hipError_t run_bwd_kernel(bool causal, const BwdArgs& a) {
 // narrower.
 template <int MODE, int ACT, bool DK>
 hipError_t launch_bwd_unit(int da, int db, bool causal, const BwdArgs& a) {
-#define STREAMKL_CASE(DA, DB)                                                                     \
-  if (da == DA && db == DB) {                                                                     \
-    if (a.dra != DA || a.drb != DB) return run_bwd_kernel<DA, DB, MODE, ACT, DK, true>(causal, a); \
-    return run_bwd_kernel<DA, DB, MODE, ACT, DK, false>(causal, a);                               \
+#define STREAMKL_CASE(DA, DB)                                                                       \
+  if (da == DA && db == DB) {                                                                       \
+    if constexpr (MODE == 3 && DA + DB >= kSplitPairsDims) {                                        \
+      return hipErrorInvalidValue; /* the host runs modes 1 and 2 instead */                        \
+    } else {                                                                                        \
+      if (a.dra != DA || a.drb != DB) return run_bwd_kernel<DA, DB, MODE, ACT, DK, true>(causal, a); \
+      return run_bwd_kernel<DA, DB, MODE, ACT, DK, false>(causal, a);                               \
+    }                                                                                               \
   }
   STREAMKL_FOR_EACH_DIM_PAIR(STREAMKL_CASE)
 #undef STREAMKL_CASE

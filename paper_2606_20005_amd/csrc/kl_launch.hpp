@@ -49,6 +49,10 @@ hipError_t launch_fwd_sigmoid(int da, int db, bool causal, const FwdArgs& a);
 int fwd_rows_per_workgroup(int da, int db, int n_q, long long bh, bool causal, bool padded);
 // Rows per workgroup of the split-K merge.
 int fwd_merge_rows_per_workgroup();
+// Kernel head dims d1 + d2 from which the host runs all four gradients as
+// the student-pair kernels followed by the teacher-pair kernels: a kernel
+// holding both pairs' accumulators would spill there (and is not built).
+constexpr int kSplitPairsDims = 448;
 hipError_t launch_bwd_dq(int da, int db, bool causal, int mode, const BwdArgs& a);
 hipError_t launch_bwd_dk(int da, int db, bool causal, int mode, const BwdArgs& a);
 // Floats of the prepared row statistics of the dK kernel (kl_bwd_rowstats_kernel):
