@@ -13,19 +13,21 @@
 // bounds the number of additions any fp32 running sum takes.
 //
 // Arithmetic is in the base-2 domain (Sec. 5 uses exp2): t = raw * s * log2(e),
-// p = 2^(t - m), and acc = sum p_a (t_a - t_b) (eq:acc-invariant in base 2, so
-// acc * ln 2 is the paper's acc). Per element: one fma and one exp2 per
-// distribution, two adds and a sub + fma for acc, plus half a max3 per
-// distribution for the tile maximum.
+// p = 2^(t - u) for an exponent reference u, and acc = sum p_a (t_a - t_b)
+// (eq:acc-invariant in base 2, so acc * ln 2 is the paper's acc). Per
+// element: one fma and one exp2 per distribution, two adds and a sub + fma
+// for acc. The tile maxima and the rescaling of Algorithm 1 run only when a
+// row's reference has to move (the lazy reference, below).
 //
 // Masking. Causal key tiles past a row block's frontier are never loaded.
 // On tiles that cross the diagonal or the ragged key tail, the raw logits of
 // keys a row may not see are replaced by kMaskedRaw, a finite stand-in for
 // -inf: such a key gets p = 2^(c * kMaskedRaw - m) = 0 exactly and a finite
 // log-ratio, so p * (x_a - x_b) = 0 and the update needs no per-key test.
-// A half-wave whose keys so far were all masked has a maximum below
-// kNoKeyRaw and takes 0 as its exponent reference. This needs |raw logits| <
-// 1e29 and s * log2(e) * 1e30 finite, far beyond any bf16 attention input.
+// In the exact update a half-wave whose keys so far were all masked has a
+// maximum below kNoKeyRaw and takes 0 as its exponent reference. This needs
+// |raw logits| < 1e29 and s * log2(e) * 1e30 finite, far beyond any bf16
+// attention input.
 //
 // "a" is the distribution in the first KL slot, "b" the second: the host
 // passes (Q1,K1) as a for KL(P1||P2) and swaps the roles for KL(P2||P1).
@@ -57,16 +59,10 @@ struct RowState {
   float mra, la, mrb, lb, acc;
 };
 
-// The online update of a tile runs in two parts: the first forms the new
-// maxima and handles keys of registers 0 .. kFirstPart - 1, the second the
-// rest. The split balances the instruction counts of the two parts.
-constexpr int kFirstPart = 7;
-
-// What the first part of a tile update hands over to the second part. The
-// all-zero carry makes a second part on a fully masked tile a no-op.
+// Per-tile values of the update: the negated exponent references and the
+// tile's partial sums (two interleaved chains each).
 struct TileCarry {
-  float ua, ub;   // scaled maxima used as exponent references for this tile
-  float aa, ab;   // correction factors of the running sums
+  float ua, ub;   // negated exponent references of this tile
   float la[2], lb[2], ac[2];
 };
 
@@ -85,8 +81,8 @@ __device__ __forceinline__ void mask_tile(f32x16& sa, f32x16& sb, int kbase, int
 
 __device__ __forceinline__ void fwd_element(TileCarry& tc, float ra, float rb, float ca, float cb, int slot,
                                             bool first) {
-  const float xa = __builtin_fmaf(ra, ca, -tc.ua);
-  const float xb = __builtin_fmaf(rb, cb, -tc.ub);
+  const float xa = __builtin_fmaf(ra, ca, tc.ua);
+  const float xb = __builtin_fmaf(rb, cb, tc.ub);
   const float pa = exp2_fast(xa);
   const float pb = exp2_fast(xb);
   const float d = xa - xb;
@@ -101,41 +97,60 @@ __device__ __forceinline__ void fwd_element(TileCarry& tc, float ra, float rb, f
   }
 }
 
-// First part of the online update of one tile (Algorithm 1): new row maxima
-// over all 16 keys of the lane, correction factors, and keys of registers
-// 0 .. kFirstPart - 1.
-__device__ __forceinline__ void fwd_update_first(RowState& st, TileCarry& tc, const f32x16& sa, const f32x16& sb,
-                                                 float ca, float cb) {
-  float xa = st.mra, xb = st.mrb;
-#pragma unroll
-  for (int i = 0; i < 16; i += 2) {
-    xa = fmaxf(fmaxf(xa, sa[i]), sa[i + 1]);
-    xb = fmaxf(fmaxf(xb, sb[i]), sb[i + 1]);
-  }
-  const float ua = xa < kNoKeyRaw ? 0.f : ca * xa;
-  const float ub = xb < kNoKeyRaw ? 0.f : cb * xb;
-  tc.ua = ua;
-  tc.ub = ub;
-  // 2^(m_old - m_new); 0 while m_old is -inf or a masked stand-in
-  tc.aa = exp2_fast(__builtin_fmaf(ca, st.mra, -ua));
-  tc.ab = exp2_fast(__builtin_fmaf(cb, st.mrb, -ub));
-  st.mra = xa;
-  st.mrb = xb;
-#pragma unroll
-  for (int i = 0; i < kFirstPart; ++i) fwd_element(tc, sa[i], sb[i], ca, cb, i & 1, i < 2);
-}
+// Lazy exponent reference. The running sums of a row stay exact for any
+// exponent reference that is actually applied, as long as every term
+// 2^(x - u) and every sum stays in the fp32 range: the reference need not be
+// the running maximum. So each tile is first reduced against the references
+// the state already holds (u = c m, m the raw maximum at the last exact
+// update), without its maxima and without rescaling. A masked key still gives
+// 0: its stand-in logit lies about 1e30 below any real reference. A lane
+// keeps that result only if both tile sums are at most kLazySumMax, which
+// also rules out inf and NaN, and a half-wave with no reference yet (m = -inf)
+// always overflows. A wave with a lane that fails forms the tile's logits
+// again from the stage and runs the exact update on the failing lanes alone:
+// the first tile of every pass, and a tile whose keys rise more than about 64
+// doublings above the reference. A row's result depends on its own data only.
+constexpr float kLazySumMax = 0x1p64f;
 
-// Second part: keys of registers kFirstPart .. 15, then fold the tile into the
-// state.
-__device__ __forceinline__ void fwd_update_second(RowState& st, TileCarry& tc, const f32x16& sa, const f32x16& sb,
-                                                  float ca, float cb) {
+// Online update of one tile (Algorithm 1). exact (wave-uniform): form the new
+// row maxima over the lane's 16 keys and rescale the sums to them first;
+// otherwise reduce against the held references. Returns whether the lane
+// took the tile. tc.ua, tc.ub hold the negated references -u.
+__device__ __forceinline__ bool fwd_update(RowState& st, TileCarry& tc, const f32x16& sa, const f32x16& sb,
+                                           float ca, float cb, bool exact) {
+  if (exact) {
+    float xa = st.mra, xb = st.mrb;
 #pragma unroll
-  for (int i = kFirstPart; i < 16; ++i) fwd_element(tc, sa[i], sb[i], ca, cb, i & 1, false);
-  const float tla = tc.la[0] + tc.la[1];
-  st.la = __builtin_fmaf(tc.aa, st.la, tla);
-  st.lb = __builtin_fmaf(tc.ab, st.lb, tc.lb[0] + tc.lb[1]);
+    for (int i = 0; i < 16; i += 2) {
+      xa = fmaxf(fmaxf(xa, sa[i]), sa[i + 1]);
+      xb = fmaxf(fmaxf(xb, sb[i]), sb[i + 1]);
+    }
+    tc.ua = xa < kNoKeyRaw ? 0.f : -ca * xa;
+    tc.ub = xb < kNoKeyRaw ? 0.f : -cb * xb;
+    // 2^(m_old - m_new); 0 while m_old is -inf or a masked stand-in
+    const float aa = exp2_fast(__builtin_fmaf(ca, st.mra, tc.ua));
+    const float ab = exp2_fast(__builtin_fmaf(cb, st.mrb, tc.ub));
+    // a half-wave with no visible key yet keeps -inf, so that a lazy pass on
+    // it overflows and falls back to this update
+    st.mra = xa < kNoKeyRaw ? kNegInf : xa;
+    st.mrb = xb < kNoKeyRaw ? kNegInf : xb;
+    st.la *= aa;
+    st.lb *= ab;
+    st.acc *= aa;
+  } else {
+    tc.ua = -ca * st.mra;
+    tc.ub = -cb * st.mrb;
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) fwd_element(tc, sa[i], sb[i], ca, cb, i & 1, i < 2);
+  const float tla = tc.la[0] + tc.la[1], tlb = tc.lb[0] + tc.lb[1];
+  const bool ok = exact || fmaxf(tla, tlb) <= kLazySumMax;
   // sum p_a (t_a - t_b) = sum p_a (x_a - x_b) + (u_a - u_b) sum p_a
-  st.acc = __builtin_fmaf(tc.aa, st.acc, __builtin_fmaf(tc.ua - tc.ub, tla, tc.ac[0] + tc.ac[1]));
+  const float dacc = __builtin_fmaf(tc.ub - tc.ua, tla, tc.ac[0] + tc.ac[1]);
+  st.la = ok ? st.la + tla : st.la;
+  st.lb = ok ? st.lb + tlb : st.lb;
+  st.acc = ok ? st.acc + dacc : st.acc;
+  return ok;
 }
 
 // S^T of one key tile on the MFMA: A = key rows from LDS, B = the lane's
@@ -143,7 +158,7 @@ __device__ __forceinline__ void fwd_update_second(RowState& st, TileCarry& tc, c
 // is in the row-padded layout and base_a, base_b are the lane's operand
 // bases (chunk slots); otherwise it is swizzled and the addresses are
 // recomputed here.
-template <int DA, int DB, bool PAD>
+template <int DA, int DB, bool PAD, int LA = 4>
 __device__ __forceinline__ void fwd_logits(const u32x4* stage, const bf16x8 (&qa)[DA / 16],
                                            const bf16x8 (&qb)[DB / 16], f32x16& sa, f32x16& sb, int lane,
                                            int base_a, int base_b) {
@@ -172,9 +187,10 @@ __device__ __forceinline__ void fwd_logits(const u32x4* stage, const bf16x8 (&qa
       if (ks < KB) acc_b = mfma32(lds_row8<CB>(tb, r, 2 * ks + half), qb[ks], acc_b);
     }
   }
-  // Keep LOOKAHEAD operand reads in flight ahead of the MFMA that consumes
-  // them: with one logits wave per SIMD nothing else hides the LDS latency.
-  constexpr int NM = KA + KB, LOOKAHEAD = NM < 4 ? NM : 4;
+  // Keep LOOKAHEAD (at most LA) operand reads in flight ahead of the MFMA
+  // that consumes them: with one logits wave per SIMD nothing else hides the
+  // LDS latency.
+  constexpr int NM = KA + KB, LOOKAHEAD = NM < LA ? NM : LA;
   __builtin_amdgcn_sched_group_barrier(0x100, LOOKAHEAD, 0);   // LDS reads
 #pragma unroll
   for (int i = 0; i < NM - LOOKAHEAD; ++i) {
@@ -263,7 +279,8 @@ __device__ __forceinline__ void write_row(const RowPartial& p, size_t ri, float*
 // SoftmaxRows keeps the five running scalars of Algorithm 1; SigmoidRows
 // keeps the sums of the sigmoid-score divergence. Each provides: State
 // (what a lane carries across tiles), Partial (what it stores, merges and
-// returns), init, update (one tile), partial, merge, and the NTOT floats per
+// returns), init, reset (start a chunk), update (one tile, lazy or exact;
+// returns whether the lane took it), partial, merge, and the NTOT floats per
 // thread that a chunk total takes in LDS.
 struct SoftmaxRows {
   static constexpr int NTOT = 5;
@@ -273,10 +290,12 @@ struct SoftmaxRows {
   };
   typedef RowPartial Partial;
   __device__ __forceinline__ static State init() { return State{RowState{kNegInf, 0.f, kNegInf, 0.f, 0.f}, {}}; }
-  __device__ __forceinline__ static void reset(State& s) { s.st = RowState{kNegInf, 0.f, kNegInf, 0.f, 0.f}; }
-  __device__ __forceinline__ static void update(State& s, const f32x16& sa, const f32x16& sb, float ca, float cb) {
-    fwd_update_first(s.st, s.tc, sa, sb, ca, cb);
-    fwd_update_second(s.st, s.tc, sa, sb, ca, cb);
+  // a new chunk keeps the exponent references (any applied reference is exact)
+  __device__ __forceinline__ static void reset(State& s) { s.st = RowState{s.st.mra, 0.f, s.st.mrb, 0.f, 0.f}; }
+  // exact = false: the lazy update; returns whether this lane took the tile
+  __device__ __forceinline__ static bool update(State& s, const f32x16& sa, const f32x16& sb, float ca, float cb,
+                                                bool exact) {
+    return fwd_update(s.st, s.tc, sa, sb, ca, cb, exact);
   }
   __device__ __forceinline__ static Partial partial(const State& s, float ca, float cb) {
     return state_partial(s.st, ca, cb);
@@ -313,7 +332,9 @@ struct SigmoidRows {
   typedef SigmoidPartial Partial;
   __device__ __forceinline__ static State init() { return State{0.f, 0.f, 0.f, 0.f}; }
   __device__ __forceinline__ static void reset(State& s) { s = init(); }
-  __device__ __forceinline__ static void update(State& s, const f32x16& sa, const f32x16& sb, float ca, float cb) {
+  // no reference to keep: every tile is taken
+  __device__ __forceinline__ static bool update(State& s, const f32x16& sa, const f32x16& sb, float ca, float cb,
+                                                bool) {
     float acc[2] = {0.f, 0.f}, dif[2] = {0.f, 0.f}, ma[2] = {0.f, 0.f}, mb[2] = {0.f, 0.f};
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
@@ -328,6 +349,7 @@ struct SigmoidRows {
     s.dif += dif[0] + dif[1];
     s.ma += ma[0] + ma[1];
     s.mb += mb[0] + mb[1];
+    return true;
   }
   __device__ __forceinline__ static Partial partial(const State& s, float, float) { return s; }
   __device__ __forceinline__ static Partial merge(const Partial& x, const Partial& y) {
@@ -472,7 +494,17 @@ __device__ __forceinline__ typename Rows::Partial fwd_pass(u32x4* st0, u32x4* st
       f32x16 sa, sb;
       fwd_logits<DA, DB, C::PAD>(cur, qa, qb, sa, sb, lane, base_a, base_b);
       if (t >= wt.tmask) mask_tile(sa, sb, t * BK + 4 * half, NK, kcm);
-      Rows::update(st, sa, sb, ca, cb);
+      const bool ok = Rows::update(st, sa, sb, ca, cb, false);
+      if (__builtin_amdgcn_ballot_w64(!ok) != 0) {   // uniform over the wave; rare
+        // Form the logits again from the stage (still in LDS) rather than
+        // keep the first ones live across the lazy pass (the barrier keeps
+        // the compiler from reusing them); one operand read ahead keeps this
+        // path within the register budget of four waves per SIMD.
+        asm volatile("" ::: "memory");
+        fwd_logits<DA, DB, C::PAD, 1>(cur, qa, qb, sa, sb, lane, base_a, base_b);
+        if (t >= wt.tmask) mask_tile(sa, sb, t * BK + 4 * half, NK, kcm);
+        if (!ok) Rows::update(st, sa, sb, ca, cb, true);
+      }
     }
     if ((t - t_begin) % kFoldTiles == kFoldTiles - 1 && t + 1 < t_end) {
       typename Rows::Partial r = Rows::partial(st, ca, cb);

@@ -69,6 +69,33 @@ def test_ragged_shapes(gpu_lib, nq, nk, causal):
     run_case(gpu_lib, d, causal, 0)
 
 
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("late", [False, True])
+def test_exponent_reference_moves_far_mid_row(gpu_lib, causal, late):
+    """Key rows scaled by 64 (exact in bf16) put the logits of some query rows
+    about 90 doublings per standard deviation away from everything else, in
+    either direction depending on the row: rows whose dot product with them
+    is positive have to move their exponent reference far up in the middle of
+    the pass (late: keys 200-215, after six tiles), lane by lane, while other
+    rows of the same waves do not; with the big keys first (late = False) the
+    later keys fall far below the reference. The single-pass forward, the
+    split forward (three chunks) and the gradients match the oracle."""
+    import torch
+    d = inputs.make("tiny", B=1, H=2, n_q=96, n_k=320)
+    big = slice(200, 216) if late else slice(0, 16)
+    d["K1"][:, :, big] *= np.float32(64.0)
+    d["K2"][:, :, 100:104] *= np.float32(64.0)
+    run_case(gpu_lib, d, causal, 0)
+    w = d["w"]
+    q1, k1, q2, k2 = upload(d)
+    kl, l1, l2 = gpu_lib.fwd_split(q1, k1, q2, k2, w.s1, w.s2, causal, 0, splits=3)
+    torch.cuda.synchronize()
+    ref = oracle.backward(d["Q1"], d["K1"], d["Q2"], d["K2"], w.s1, w.s2, causal, 0, d["g"])
+    check_rows("kl split", kl.cpu().numpy(), ref[0])
+    check_rows("lse1 split", l1.cpu().numpy(), ref[1])
+    check_rows("lse2 split", l2.cpu().numpy(), ref[2])
+
+
 @pytest.mark.parametrize("d1", [64, 128, 192, 256])
 @pytest.mark.parametrize("d2", [64, 128, 192, 256])
 def test_every_head_dim_pair(gpu_lib, d1, d2):
