@@ -22,7 +22,7 @@
 // Masking. Causal key tiles past a row block's frontier are never loaded.
 // On tiles that cross the diagonal or the ragged key tail, the raw logits of
 // keys a row may not see are replaced by kMaskedRaw, a finite stand-in for
-// -inf: such a key gets p = 2^(c * kMaskedRaw - m) = 0 exactly and a finite
+// -inf: such a key gets p = 2^(c * kMaskedRaw - u) = 0 exactly and a finite
 // log-ratio, so p * (x_a - x_b) = 0 and the update needs no per-key test.
 // In the exact update a half-wave whose keys so far were all masked has a
 // maximum below kNoKeyRaw and takes 0 as its exponent reference. This needs
@@ -52,9 +52,10 @@ constexpr int kFwdBK = 32;             // key rows per tile (one 32x32 MFMA bloc
 constexpr float kMaskedRaw = -1e30f;   // raw logit of a key the row may not see
 constexpr float kNoKeyRaw = -5e29f;    // maxima below this mean "no visible key yet"
 
-// Five running row scalars of one half-wave. The maxima are kept in raw
-// dot-product units (s > 0, so the scaled maximum is c * m); l and acc are
-// relative to 2^(c * m) (base-2 domain, see above).
+// Five running row scalars of one half-wave. mra, mrb: the raw maximum at
+// the last exact update (s > 0, so the scaled one is c * m), -inf while the
+// half-wave has seen no visible key; it sets the exponent reference u = c m,
+// and l and acc are relative to 2^u (base-2 domain, see above).
 struct RowState {
   float mra, la, mrb, lb, acc;
 };
