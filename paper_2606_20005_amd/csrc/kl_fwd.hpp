@@ -154,21 +154,21 @@ __device__ __forceinline__ bool fwd_update(RowState& st, TileCarry& tc, const f3
   return ok;
 }
 
-// S^T of one key tile on the MFMA: A = key rows from LDS, B = the lane's
-// resident query rows; the two accumulation chains alternate. PAD: the tile
-// is in the row-padded layout and base_a, base_b are the lane's operand
-// bases (chunk slots); otherwise it is swizzled and the addresses are
-// recomputed here.
+// S^T of one key tile on the MFMA: A = key rows from LDS (the tile's rows of
+// K_a from tile_a, of K_b from tile_b), B = the lane's resident query rows;
+// the two accumulation chains alternate. PAD: the tile is in the row-padded
+// layout and base_a, base_b are the lane's operand bases (chunk slots);
+// otherwise it is swizzled and the addresses are recomputed here.
 template <int DA, int DB, bool PAD, int LA = 4>
-__device__ __forceinline__ void fwd_logits(const u32x4* stage, const bf16x8 (&qa)[DA / 16],
+__device__ __forceinline__ void fwd_logits(const u32x4* tile_a, const u32x4* tile_b, const bf16x8 (&qa)[DA / 16],
                                            const bf16x8 (&qb)[DB / 16], f32x16& sa, f32x16& sb, int lane,
                                            int base_a, int base_b) {
   constexpr int KA = DA / 16, KB = DB / 16, KM = KA > KB ? KA : KB;
   constexpr int CA = DA / 8, CB = DB / 8;
   f32x16 acc_a = zero16(), acc_b = zero16();
   if constexpr (PAD) {
-    const u32x4* ta = stage + base_a;
-    const u32x4* tb = stage + kFwdBK * PadRows<CA>::P + base_b;
+    const u32x4* ta = tile_a + base_a;
+    const u32x4* tb = tile_b + base_b;
 #pragma unroll
     for (int ks = 0; ks < KM; ++ks) {
       if (ks < KA) acc_a = mfma32(__builtin_bit_cast(bf16x8, ta[ks]), qa[ks], acc_a);
@@ -180,8 +180,8 @@ __device__ __forceinline__ void fwd_logits(const u32x4* stage, const bf16x8 (&qa
     // them live across the loop: the update state has no registers to spare.
     int r = lane & 31;
     asm volatile("" : "+v"(r));
-    const u32x4* ta = stage;
-    const u32x4* tb = stage + kFwdBK * CA;
+    const u32x4* ta = tile_a;
+    const u32x4* tb = tile_b;
 #pragma unroll
     for (int ks = 0; ks < KM; ++ks) {
       if (ks < KA) acc_a = mfma32(lds_row8<CA>(ta, r, 2 * ks + half), qa[ks], acc_a);
@@ -401,29 +401,35 @@ __device__ __forceinline__ WaveTiles wave_tiles(int qw, int wlast, int NQ, int N
 }
 
 // ----------------------------------------------------------------------------
-// Forward kernel. A workgroup of NW waves owns 32 * NW query rows and streams
-// the key tiles once for all of them (the first DMA_NT threads issue the
-// loads); each wave forms and reduces its own tiles. Iteration t forms and
-// reduces tile t from its stage while tile t + NSTAGE - 1 streams into the
-// stage tile t - 1 occupied; after tile t + 1 has landed, (NSTAGE - 2) tiles
-// of loads are still in flight.
+// Forward kernel. A workgroup of NW waves owns 32 * NW / KS query rows and
+// streams the key tiles once for all of them (the first DMA_NT threads issue
+// the loads). With KS = 1 each wave forms and reduces every tile for its 32
+// rows. With KS = 2 a ring stage holds two consecutive tiles and the waves
+// split in two halves over the same rows: wave w (row group w % RG) takes the
+// first tile of each stage when w < RG, the second otherwise, and the two
+// halves merge their row states once at the end by the split-K rule. Stage
+// iteration u forms and reduces stage u while stage u + NSTAGE - 1 streams
+// into the buffer stage u - 1 occupied.
 // ----------------------------------------------------------------------------
-template <int DA_, int DB_, int NSTAGE_, int MINB_, int NW_ = 4, bool PAD_ = false>
+template <int DA_, int DB_, int NSTAGE_, int MINB_, int NW_ = 4, bool PAD_ = false, int KS_ = 1>
 struct FwdTraits {
   static constexpr int DA = DA_, DB = DB_;
   static constexpr int NW = NW_;                            // waves per workgroup
   static constexpr int NT = 64 * NW;
-  static constexpr int BQ = 32 * NW;                        // query rows per workgroup
+  static constexpr int KS = KS_;                            // key tiles per ring stage, one per wave half
+  static constexpr int RG = NW / KS;                        // row groups of 32 rows
+  static constexpr int BQ = 32 * RG;                        // query rows per workgroup
   static constexpr int BK = kFwdBK;
+  static constexpr int ROWS = BK * KS;                      // key rows per ring stage
   static constexpr int CA = DA / 8, CB = DB / 8;
   // key tiles in the row-padded layout (one operand base register) or swizzled
   static constexpr bool PAD = PAD_;
   static constexpr int SA = PAD ? PadRows<CA>::P : CA, SB = PAD ? PadRows<CB>::P : CB;   // slots per row
-  static constexpr int STAGE = BK * (SA + SB);
+  static constexpr int STAGE = ROWS * (SA + SB);
   static constexpr int NSTAGE = NSTAGE_;
   // threads that stream the key tiles: the most (of 512, 384, 256, 128, 64, up to the workgroup) that split both
   // tensors' slots into whole loads
-  static constexpr bool splits(int n) { return n <= NT && (BK * SA) % n == 0 && (BK * SB) % n == 0; }
+  static constexpr bool splits(int n) { return n <= NT && (ROWS * SA) % n == 0 && (ROWS * SB) % n == 0; }
   static constexpr int DMA_NT = splits(512) ? 512 : splits(384) ? 384 : splits(256) ? 256 : splits(128) ? 128 : 64;
   static constexpr int NCH = STAGE / DMA_NT;                // direct-to-LDS loads per streaming thread per tile
   static constexpr int MINB = MINB_;                        // workgroups per CU the registers are sized for
@@ -433,25 +439,31 @@ struct FwdTraits {
   static constexpr int WAVES_PER_SIMD = (MINB * NW + 3) / 4;
   static_assert(DA % 64 == 0 && DB % 64 == 0, "head dims must be multiples of 64");
   static_assert(NSTAGE >= 2, "tile shape");
+  static_assert(KS == 1 || KS == 2, "one or two key tiles per stage");
+  static_assert(NW % KS == 0, "wave halves");
 };
 
 // Online pass of one workgroup over key tiles [t_begin, t_end) of the query
 // rows q0 .. q0 + BQ - 1 of head bh; returns the lane's row state (both
-// half-waves merged) and its row index in myq. tot: LDS for the per-lane
-// totals of the chunked sums, 5 * NT floats.
+// half-waves merged, and with KS = 2 both wave halves) and its row index in
+// myq; owner: whether this wave writes the rows (the first wave half). tot:
+// LDS for the per-lane totals of the chunked sums, NTOT * NT floats. With
+// KS = 2, t_begin must be a multiple of 2 (the single pass starts at 0).
 template <class C, bool CAUSAL, class Rows = SoftmaxRows>
 __device__ __forceinline__ typename Rows::Partial fwd_pass(u32x4* st0, u32x4* st1, float* tot,
                                                            const uint16_t* __restrict__ Qa,
                                                const uint16_t* __restrict__ Ka, const uint16_t* __restrict__ Qb,
                                                const uint16_t* __restrict__ Kb, int NQ, int NK, int dra, int drb,
                                                float ca, float cb, int bh, int q0, int t_begin, int t_end,
-                                               int& myq) {
-  constexpr int DA = C::DA, DB = C::DB, BK = C::BK;
+                                               int& myq, bool& owner) {
+  constexpr int DA = C::DA, DB = C::DB, BK = C::BK, KS = C::KS;
   static_assert(C::NSTAGE == 2, "the tile loop names two stage arrays");
   const int tid = threadIdx.x, lane = tid & 63, half = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int rg = wave % C::RG, kslot = wave / C::RG;   // row group, and which tile of a stage
+  owner = kslot == 0;
   const int off = NK - NQ;
-  const int qw = q0 + 32 * wave;
+  const int qw = q0 + 32 * rg;
   myq = qw + (lane & 31);
   const int wlast = min(qw + 31, NQ - 1);
 
@@ -462,6 +474,7 @@ __device__ __forceinline__ typename Rows::Partial fwd_pass(u32x4* st0, u32x4* st
   }
   const WaveTiles wt = wave_tiles<CAUSAL>(qw, wlast, NQ, NK, ntiles);
   t_end = min(t_end, ntiles);
+  const int u_begin = t_begin / KS, u_end = (t_end + KS - 1) / KS;   // ring stages
   const int kcm = CAUSAL ? myq + off : NK;
 
   bf16x8 qa[DA / 16], qb[DB / 16];
@@ -470,30 +483,34 @@ __device__ __forceinline__ typename Rows::Partial fwd_pass(u32x4* st0, u32x4* st
 
   const rsrc_t rka = make_rsrc(Ka + (size_t)bh * NK * dra, (uint32_t)NK * dra * 2u);
   const rsrc_t rkb = make_rsrc(Kb + (size_t)bh * NK * drb, (uint32_t)NK * drb * 2u);
-  using Dma = typename std::conditional<C::PAD, PadTileDma<BK, C::CA, C::CB, C::DMA_NT>,
-                                        TileDma<BK, C::CA, C::CB, C::DMA_NT>>::type;
+  using Dma = typename std::conditional<C::PAD, PadTileDma<C::ROWS, C::CA, C::CB, C::DMA_NT>,
+                                        TileDma<C::ROWS, C::CA, C::CB, C::DMA_NT>>::type;
   const bool streamer = wave < C::DMA_NT / 64;
   const Dma dma(streamer ? tid : 0, dra / 8, drb / 8);
   // operand bases of the row-padded layout (unused otherwise)
   const int base_a = C::PAD ? PadRows<C::CA>::base(lane & 31, half) : 0;
   const int base_b = C::PAD ? PadRows<C::CB>::base(lane & 31, half) : 0;
+  // this wave's tile within a stage: rows kslot * BK .. of each tensor (both
+  // layouts repeat their slot pattern every 16 rows)
+  const int tile_a = kslot * BK * C::SA, tile_b = C::ROWS * C::SA + kslot * BK * C::SB;
   typename Rows::State st = Rows::init();
   bool have_total = false;   // uniform: whether tot holds a chunk yet
 
-  if (t_begin < t_end && streamer) {
-    dma.issue(rka, rkb, t_begin * BK, st0, wave, dra, drb);
-    wait_vmem();   // tile t_begin
+  if (u_begin < u_end && streamer) {
+    dma.issue(rka, rkb, u_begin * C::ROWS, st0, wave, dra, drb);
+    wait_vmem();   // stage u_begin
   }
   barrier_no_fence();
-  // One tile: cur holds tile t, the next tile streams into nxt. The two ring
-  // stages are separate arrays named by the loop (two tiles per trip), so
-  // the compiler can tell that a tile's reads never touch the stage being
+  // One stage: cur holds stage u, the next stage streams into nxt. The two
+  // ring stages are separate arrays named by the loop (two stages per trip),
+  // so the compiler can tell that a stage's reads never touch the stage being
   // loaded (and inserts no wait for those loads).
-  auto step = [&](const u32x4* cur, u32x4* nxt, int t) {
-    if (streamer) dma.issue(rka, rkb, (t + 1) * BK, nxt, wave, dra, drb);
-    if (t <= wt.tlast) {
+  auto step = [&](const u32x4* cur, u32x4* nxt, int u) {
+    if (streamer) dma.issue(rka, rkb, (u + 1) * C::ROWS, nxt, wave, dra, drb);
+    const int t = u * KS + kslot;   // this wave's key tile
+    if (t <= wt.tlast && (KS == 1 || t < t_end)) {
       f32x16 sa, sb;
-      fwd_logits<DA, DB, C::PAD>(cur, qa, qb, sa, sb, lane, base_a, base_b);
+      fwd_logits<DA, DB, C::PAD>(cur + tile_a, cur + tile_b, qa, qb, sa, sb, lane, base_a, base_b);
       if (t >= wt.tmask) mask_tile(sa, sb, t * BK + 4 * half, NK, kcm);
       const bool ok = Rows::update(st, sa, sb, ca, cb, false);
       if (__builtin_amdgcn_ballot_w64(!ok) != 0) {   // uniform over the wave; rare
@@ -502,29 +519,37 @@ __device__ __forceinline__ typename Rows::Partial fwd_pass(u32x4* st0, u32x4* st
         // the compiler from reusing them); one operand read ahead keeps this
         // path within the register budget of four waves per SIMD.
         asm volatile("" ::: "memory");
-        fwd_logits<DA, DB, C::PAD, 1>(cur, qa, qb, sa, sb, lane, base_a, base_b);
+        fwd_logits<DA, DB, C::PAD, 1>(cur + tile_a, cur + tile_b, qa, qb, sa, sb, lane, base_a, base_b);
         if (t >= wt.tmask) mask_tile(sa, sb, t * BK + 4 * half, NK, kcm);
         if (!ok) Rows::update(st, sa, sb, ca, cb, true);
       }
     }
-    if ((t - t_begin) % kFoldTiles == kFoldTiles - 1 && t + 1 < t_end) {
+    if ((u - u_begin) % kFoldTiles == kFoldTiles - 1 && u + 1 < u_end) {
       typename Rows::Partial r = Rows::partial(st, ca, cb);
       if (have_total) r = Rows::merge(Rows::load(tot, tid, C::NT), r);
       Rows::store(tot, tid, C::NT, r);
       have_total = true;
       Rows::reset(st);
     }
-    wait_vmem();          // tile t + 1 has landed (for this wave) ...
+    wait_vmem();          // stage u + 1 has landed (for this wave) ...
     barrier_no_fence();   // ... and for every wave
   };
-  for (int t = t_begin; t < t_end; t += 2) {
-    step(st0, st1, t);
-    if (t + 1 < t_end) step(st1, st0, t + 1);
+  for (int u = u_begin; u < u_end; u += 2) {
+    step(st0, st1, u);
+    if (u + 1 < u_end) step(st1, st0, u + 1);
   }
   wait_vmem();   // no load may still target LDS when the workgroup ends
   typename Rows::Partial mine = Rows::partial(st, ca, cb);
   if (have_total) mine = Rows::merge(Rows::load(tot, tid, C::NT), mine);
-  return Rows::halfwave(mine);
+  mine = Rows::halfwave(mine);
+  if constexpr (KS == 2) {
+    // the second wave half hands its rows' states to the first through its
+    // own total slots
+    if (!owner) Rows::store(tot, tid, C::NT, mine);
+    __syncthreads();
+    if (owner) mine = Rows::merge(mine, Rows::load(tot, tid + 64 * C::RG, C::NT));
+  }
+  return mine;
 }
 
 // Whole key range per workgroup: grid B*H * ceil(N_Q / BQ).
@@ -548,10 +573,11 @@ kl_fwd_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restrict__ Ka,
   head_block<CAUSAL, C::MINB>(TQ, bh, qt);
   if (CAUSAL) qt = TQ - 1 - qt;   // rank 0: the last rows, the longest
   int myq;
+  bool owner;
   const RowPartial p =
       fwd_pass<C, CAUSAL>(st0, st1, tot, Qa, Ka, Qb, Kb, NQ, NK, dra, drb, ca, cb, bh, qt * C::BQ, 0, 1 << 30,
-                          myq);
-  if ((threadIdx.x & 32) == 0 && myq < NQ) write_row(p, (size_t)bh * NQ + myq, kl, lse_a, lse_b);
+                          myq, owner);
+  if ((threadIdx.x & 32) == 0 && owner && myq < NQ) write_row(p, (size_t)bh * NQ + myq, kl, lse_a, lse_b);
 }
 
 // Forward of the sigmoid-score divergence (see SigmoidRows): the same tile
@@ -576,9 +602,10 @@ kl_fwd_sigmoid_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restric
   head_block<CAUSAL, C::MINB>(TQ, bh, qt);
   if (CAUSAL) qt = TQ - 1 - qt;   // rank 0: the last rows, the longest
   int myq;
+  bool owner;
   const SigmoidPartial p = fwd_pass<C, CAUSAL, SigmoidRows>(st0, st1, tot, Qa, Ka, Qb, Kb, NQ, NK, dra, drb, ca, cb,
-                                                            bh, qt * C::BQ, 0, 1 << 30, myq);
-  if ((threadIdx.x & 32) == 0 && myq < NQ) write_row_sigmoid(p, (size_t)bh * NQ + myq, kl, mass_a, mass_b);
+                                                            bh, qt * C::BQ, 0, 1 << 30, myq, owner);
+  if ((threadIdx.x & 32) == 0 && owner && myq < NQ) write_row_sigmoid(p, (size_t)bh * NQ + myq, kl, mass_a, mass_b);
 }
 
 // Split-K partial pass (Sec. 3.3): grid B*H * ceil(N_Q / BQ) * W; workgroup
@@ -605,9 +632,11 @@ kl_fwd_partial_kernel(const uint16_t* __restrict__ Qa, const uint16_t* __restric
   const int rest = logical / W;
   const int bh = rest / TQ;
   const int qt = rest - bh * TQ;
+  static_assert(C::KS == 1, "chunks of single key tiles");
   int myq;
+  bool owner;
   const RowPartial p = fwd_pass<C, CAUSAL>(st0, st1, tot, Qa, Ka, Qb, Kb, NQ, NK, dra, drb, ca, cb, bh, qt * C::BQ,
-                                           w * chunk, (w + 1) * chunk, myq);
+                                           w * chunk, (w + 1) * chunk, myq, owner);
   if ((threadIdx.x & 32) == 0 && myq < NQ) {
     const size_t rows = (size_t)gridDim.x / W / TQ * NQ;   // B*H*N_Q
     const size_t ri = (size_t)w * rows + (size_t)bh * NQ + myq;
@@ -666,6 +695,15 @@ using FwdCfg = typename std::conditional<(DA + DB <= 256), FwdTraits<DA, DB, 2, 
 template <int DA, int DB>
 using FwdCausalSmallCfg = FwdTraits<DA, DB, 2, 2, 4, true>;
 
+// Causal grids of those that fit one round of resident workgroups (d1 + d2 <=
+// 192): the same 128 rows per workgroup as eight waves in two halves that
+// take alternate key tiles (two tiles per ring stage, swizzled layout: the
+// padded one would not leave room for two workgroups per CU). With every
+// workgroup resident at once the longest causal block sets the time, and the
+// two halves split it. Wider pairs do not fit this in 128 registers.
+template <int DA, int DB>
+using FwdCausalKeySplitCfg = FwdTraits<DA, DB, 2, 2, 8, false, 2>;
+
 // Padded head dims (32, 96, 160, 224 run as 64, 128, 192, 256): one
 // configuration for every shape, four waves and 128 rows per workgroup.
 template <int DA, int DB>
@@ -678,19 +716,26 @@ using FwdSmallCfg = FwdTraits<DA, DB, 2, (DA + DB <= 256) ? (NW == 1 ? 4 : 2) : 
 
 // Which configuration a head shape takes (the launch units instantiate
 // them): one wave for at most 32 query rows, four waves for at most 128
-// (d1 + d2 <= 256), the 128-row causal configuration when 256-row workgroups
-// would number fewer than four per CU, otherwise FwdCfg. The causal 128-row
-// configuration measured 10-16% faster on such shapes (twice the workgroups:
-// the two waves sharing a SIMD come from different workgroups and the long
-// causal rows spread over more CUs); non-causal shapes of the same size were
-// 4-6% slower with it and keep the default.
-enum class FwdShape { kOneWave, kFourWaves, kCausalSmall, kDefault };
+// (d1 + d2 <= 256), the 128-row causal configurations when 256-row
+// workgroups would number fewer than four per CU, otherwise FwdCfg. The
+// causal 128-row configuration measured 10-16% faster on such shapes (twice
+// the workgroups: the two waves sharing a SIMD come from different workgroups
+// and the long causal rows spread over more CUs); non-causal shapes of the
+// same size were 4-6% slower with it and keep the default. Of those causal
+// grids, the ones that fit one round (at most 512 workgroups of 128 rows, d1 +
+// d2 <= 192) take the key-split configuration: 7-10% faster there, about 1%
+// slower on two-round grids.
+enum class FwdShape { kOneWave, kFourWaves, kCausalSmall, kCausalKeySplit, kDefault };
 constexpr long long kCausalSmallGrid = 1024;
+constexpr long long kCausalOneRound = 512;
 inline FwdShape fwd_shape(int da, int db, int n_q, long long bh, bool causal) {
   if (n_q <= 32) return FwdShape::kOneWave;
   if (da + db <= 256) {
     if (n_q <= 128) return FwdShape::kFourWaves;
-    if (causal && bh * ((n_q + 255) / 256) < kCausalSmallGrid) return FwdShape::kCausalSmall;
+    if (causal && bh * ((n_q + 255) / 256) < kCausalSmallGrid) {
+      if (da + db <= 192 && bh * ((n_q + 127) / 128) <= kCausalOneRound) return FwdShape::kCausalKeySplit;
+      return FwdShape::kCausalSmall;
+    }
   }
   return FwdShape::kDefault;
 }

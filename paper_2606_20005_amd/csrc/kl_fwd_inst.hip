@@ -15,18 +15,22 @@ static hipError_t run_cfg(const FwdArgs& a, int W, float* part) {
                        a.Qa, a.Ka, a.Qb, a.Kb, a.NQ, a.NK, a.dra, a.drb, a.ca, a.cb, a.kl, a.lse_a, a.lse_b);
     return hipGetLastError();
   }
-  const int nkt = (a.NK + C::BK - 1) / C::BK;
-  const int chunk = (nkt + W - 1) / W;
-  const dim3 grid((unsigned)((long long)a.BH * tq * W));
-  hipLaunchKernelGGL((kl_fwd_partial_kernel<C, CAUSAL, PD>), grid, dim3(C::NT), 0, a.stream,
-                     a.Qa, a.Ka, a.Qb, a.Kb, a.NQ, a.NK, a.dra, a.drb, a.ca, a.cb, W, chunk, part);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  const size_t rows = (size_t)a.BH * a.NQ;
-  hipLaunchKernelGGL(kl_fwd_merge_kernel, dim3((unsigned)((rows + kMergeRowsPerBlock - 1) / kMergeRowsPerBlock)),
-                     dim3(64 * kMergeRowsPerBlock), 0, a.stream,
-                     part, W, rows, a.kl, a.lse_a, a.lse_b);
-  return hipGetLastError();
+  if constexpr (C::KS > 1) {
+    return hipErrorInvalidValue;   // the split pass takes configurations of one tile per stage
+  } else {
+    const int nkt = (a.NK + C::BK - 1) / C::BK;
+    const int chunk = (nkt + W - 1) / W;
+    const dim3 grid((unsigned)((long long)a.BH * tq * W));
+    hipLaunchKernelGGL((kl_fwd_partial_kernel<C, CAUSAL, PD>), grid, dim3(C::NT), 0, a.stream,
+                       a.Qa, a.Ka, a.Qb, a.Kb, a.NQ, a.NK, a.dra, a.drb, a.ca, a.cb, W, chunk, part);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const size_t rows = (size_t)a.BH * a.NQ;
+    hipLaunchKernelGGL(kl_fwd_merge_kernel, dim3((unsigned)((rows + kMergeRowsPerBlock - 1) / kMergeRowsPerBlock)),
+                       dim3(64 * kMergeRowsPerBlock), 0, a.stream,
+                       part, W, rows, a.kl, a.lse_a, a.lse_b);
+    return hipGetLastError();
+  }
 }
 
 template <int DA, int DB, bool CAUSAL>
@@ -40,6 +44,12 @@ static hipError_t run_fwd(const FwdArgs& a, int W, float* part) {
     case FwdShape::kCausalSmall:
       if constexpr (DA + DB <= 256) return run_cfg<DA, DB, CAUSAL, FwdCausalSmallCfg<DA, DB>>(a, W, part);
       break;
+    case FwdShape::kCausalKeySplit:
+      if constexpr (DA + DB <= 192) {
+        if (W <= 1) return run_cfg<DA, DB, CAUSAL, FwdCausalKeySplitCfg<DA, DB>>(a, W, part);
+        return run_cfg<DA, DB, CAUSAL, FwdCausalSmallCfg<DA, DB>>(a, W, part);   // split pass: single tiles
+      }
+      break;
     case FwdShape::kDefault: break;
   }
   return run_cfg<DA, DB, CAUSAL, FwdCfg<DA, DB>>(a, W, part);
@@ -52,7 +62,8 @@ int fwd_rows_per_workgroup(int da, int db, int n_q, long long bh, bool causal, b
   switch (fwd_shape(da, db, n_q, bh, causal)) {
     case FwdShape::kOneWave: return 32;
     case FwdShape::kFourWaves:
-    case FwdShape::kCausalSmall: return 128;
+    case FwdShape::kCausalSmall:
+    case FwdShape::kCausalKeySplit: return 128;
     case FwdShape::kDefault: break;
   }
   return da + db <= 256 ? 256 : 128;
