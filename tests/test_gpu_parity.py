@@ -69,6 +69,18 @@ def test_ragged_shapes(gpu_lib, nq, nk, causal):
     run_case(gpu_lib, d, causal, 0)
 
 
+@pytest.mark.parametrize("H,nq,nk,d1,d2", [(3, 400, 650, 128, 64), (2, 513, 513, 64, 128), (1, 129, 1000, 64, 64),
+                                           (2, 700, 300, 128, 64)])
+def test_causal_key_split_grids(gpu_lib, H, nq, nk, d1, d2):
+    """Causal grids of at most 512 workgroups of 128 rows with d1 + d2 <= 192
+    take the key-split forward (two wave halves over alternate key tiles of
+    each ring stage, merged at the end): odd numbers of key tiles, ragged key
+    tails, N_Q above and below N_K (rows with no key), all gradients."""
+    d = inputs.make("tiny", B=1, H=H, n_q=nq, n_k=nk, d1=d1, d2=d2)
+    run_case(gpu_lib, d, True, 0)
+    run_case(gpu_lib, d, True, 1, want=("dq2", "dk2"))
+
+
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("late", [False, True])
 def test_exponent_reference_moves_far_mid_row(gpu_lib, causal, late):
