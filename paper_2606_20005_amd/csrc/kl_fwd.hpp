@@ -105,9 +105,9 @@ __device__ __forceinline__ void fwd_element(TileCarry& tc, float ra, float rb, f
 // the state already holds (u = c m, m the raw maximum at the last exact
 // update), without its maxima and without rescaling. A masked key still gives
 // 0: its stand-in logit lies about 1e30 below any real reference. A lane
-// keeps that result only if both tile sums are at most kLazySumMax, which
-// also rules out inf and NaN, and a half-wave with no reference yet (m = -inf)
-// always overflows. A wave with a lane that fails forms the tile's logits
+// keeps that result only if its two tile sums add up to at most kLazySumMax,
+// which also rules out inf and NaN, and a half-wave with no reference yet
+// (m = -inf) always overflows. A wave with a lane that fails forms the tile's logits
 // again from the stage and runs the exact update on the failing lanes alone:
 // the first tile of every pass, and a tile whose keys rise more than about 64
 // doublings above the reference. A row's result depends on its own data only.
@@ -145,7 +145,8 @@ __device__ __forceinline__ bool fwd_update(RowState& st, TileCarry& tc, const f3
 #pragma unroll
   for (int i = 0; i < 16; ++i) fwd_element(tc, sa[i], sb[i], ca, cb, i & 1, i < 2);
   const float tla = tc.la[0] + tc.la[1], tlb = tc.lb[0] + tc.lb[1];
-  const bool ok = exact || fmaxf(tla, tlb) <= kLazySumMax;
+  // both sums are >= 0: their sum bounds each, and an inf or NaN in either fails
+  const bool ok = exact || tla + tlb <= kLazySumMax;
   // sum p_a (t_a - t_b) = sum p_a (x_a - x_b) + (u_a - u_b) sum p_a
   const float dacc = __builtin_fmaf(tc.ub - tc.ua, tla, tc.ac[0] + tc.ac[1]);
   st.la = ok ? st.la + tla : st.la;
