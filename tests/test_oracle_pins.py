@@ -394,3 +394,44 @@ def test_empty_partial_state_is_neutral():
             np.testing.assert_array_equal(a[k], b[k])
     kl, l1, l2 = om.finalize(om.empty_state(3))
     assert np.all(kl == 0.0) and np.all(np.isneginf(l1)) and np.all(np.isneginf(l2))
+
+
+def test_any_applied_exponent_reference_finalizes_the_same():
+    """A partial state need not be relative to its maxima: with l_t = sum
+    e^{S_t - u_t} and acc = sum e^{S1 - u1} (S1 - S2) over its keys, any
+    applied references u_t merge (Sec. 3.3) and finalize (eq:kl-final) to
+    the same KL and LSEs. The forward kernel relies on this: it reduces each
+    tile against the reference its row already holds and forms new maxima
+    only when a tile's terms would leave the fp32 range. Pinned against the
+    plain definition, causal, with each tile either keeping the previous
+    tile's reference (a merge with equal references is a plain addition, as
+    in the kernel) or taking one up to 60 nats below or above its maximum."""
+    from oracle import online_model as om
+    from oracle.kl_oracle import allowed_mask
+    n_q, n_k, bk = 24, 160, 32
+    d = inputs.make("tiny", n_q=n_q, n_k=n_k)
+    w = d["w"]
+    q1, k1, q2, k2 = (d[k][0, 0].astype(np.float64) for k in ("Q1", "K1", "Q2", "K2"))
+    rk, r1, r2 = oracle.forward(d["Q1"], d["K1"], d["Q2"], d["K2"], w.s1, w.s2, True, FWD)
+    S1, S2 = om._logits(q1, k1, q2, k2, w.s1, w.s2)
+    mask = allowed_mask(np.arange(n_q), n_q, n_k, True)
+    rng = np.random.default_rng(23)
+    st = om.empty_state(n_q)
+    for j0 in range(0, n_k, bk):
+        S1t, S2t, mt = S1[:, j0:j0 + bk], S2[:, j0:j0 + bk], mask[:, j0:j0 + bk]
+        seen = mt.any(axis=1)
+        refs = []
+        for St, held in ((S1t, st["m1"]), (S2t, st["m2"])):
+            fresh = np.where(mt, St, -np.inf).max(axis=1) + rng.uniform(-60.0, 60.0, n_q)
+            keep = rng.random(n_q) < 0.6
+            refs.append(np.where(seen, np.where(keep & np.isfinite(held), held, fresh), -np.inf))
+        u1, u2 = refs
+        e1 = np.where(mt, np.exp(np.where(mt, S1t, 0.0) - np.where(seen, u1, 0.0)[:, None]), 0.0)
+        e2 = np.where(mt, np.exp(np.where(mt, S2t, 0.0) - np.where(seen, u2, 0.0)[:, None]), 0.0)
+        tile = dict(m1=u1, l1=e1.sum(axis=1), m2=u2, l2=e2.sum(axis=1),
+                    acc=(e1 * np.where(mt, S1t - S2t, 0.0)).sum(axis=1))
+        st = om.merge_states(st, tile)
+    kl, l1, l2 = om.finalize(st)
+    np.testing.assert_allclose(kl, rk[0, 0], rtol=1e-9, atol=1e-12)
+    np.testing.assert_allclose(l1, r1[0, 0], rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(l2, r2[0, 0], rtol=1e-12, atol=1e-12)
