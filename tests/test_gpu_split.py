@@ -25,7 +25,7 @@ def run_split(sk, d, causal, direction, splits, workspace=None):
     (16, 4096, False, 0, 32),     # decode-like
     (16, 4096, True, 1, 5),       # causal bottom-right, reverse direction
     (33, 1000, True, 0, 3),       # two waves' worth of rows
-    (200, 300, True, 0, 4),       # several query workgroups
+    (200, 300, True, 0, 4),       # several query workgroups; the single pass of this shape takes the key split
     (64, 40, False, 0, 8),        # more splits than key tiles: empty chunks
     (300, 100, True, 0, 2),       # rows with no visible key (N_Q > N_K)
 ])
