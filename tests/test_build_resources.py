@@ -4,10 +4,11 @@ Compiles the forward unit and the backward units of gradient modes 1 and 3
 for the device only, with the compiler's per-kernel resource remarks, and
 checks the promises the kernel configurations make:
 
-* every forward kernel (single pass and split-K partial pass, for head dims
-  that are multiples of 64 and for padded ones) fits the workgroups per CU
-  its configuration is sized for, MINB workgroups of NW waves =
-  ceil(MINB * NW / 4) waves per SIMD, without spilling;
+* every forward kernel (single pass, split-K partial pass and the sigmoid
+  forward, for head dims that are multiples of 64 and for padded ones, and
+  the key-split configuration) fits the workgroups per CU its configuration
+  is sized for, MINB workgroups of NW waves = ceil(MINB * NW / 4) waves per
+  SIMD, without spilling;
 * the student-gradient backward kernels (mode 1) for head dims that are
   multiples of 64 never spill, and those of the workload head dims
   (128, 128), (128, 64), (192, 64) run two workgroups (two waves) per SIMD;
@@ -26,7 +27,7 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2606_20005_amd", "csrc")
-UNITS = ("kl_fwd_inst", "kl_bwd_dq_m1", "kl_bwd_dk_m1", "kl_bwd_dq_m3", "kl_bwd_dk_m3")
+UNITS = ("kl_fwd_inst", "kl_fwd_sigmoid_inst", "kl_bwd_dq_m1", "kl_bwd_dk_m1", "kl_bwd_dq_m3", "kl_bwd_dk_m3")
 
 
 def _hipcc():
@@ -71,8 +72,8 @@ def kernels(tmp_path_factory):
     return res
 
 
-# FwdTraits<DA, DB, NSTAGE, MINB, NW, PAD> in the mangled name of a forward kernel
-FWD_RE = re.compile(r"kl_fwd_(?:partial_)?kernelINS_9FwdTraitsILi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)ELb([01])")
+# FwdTraits<DA, DB, NSTAGE, MINB, NW, PAD[, KS]> in the mangled name of a forward kernel
+FWD_RE = re.compile(r"kl_fwd_(?:partial_|sigmoid_)?kernelINS_9FwdTraitsILi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)ELb([01])")
 # kl_bwd_{dq,dk}_kernel<DA, DB, CAUSAL, MODE, ACT, PD>
 BWD_RE = re.compile(r"kl_bwd_(dq|dk)_kernelILi(\d+)ELi(\d+)ELb([01])ELi(\d+)ELi(\d+)ELb([01])E")
 PD_SPILL_LIMIT = 16   # bytes per lane the padded-dim backward instantiations may spill
@@ -89,7 +90,7 @@ def test_forward_occupancy_as_configured(kernels):
         promised = (minb * nw + 3) // 4
         assert r["ScratchSize [bytes/lane]"] == 0, (da, db, minb, nw, r)
         assert r["Occupancy [waves/SIMD]"] >= promised, (da, db, minb, nw, r)
-    assert seen >= 16 * 4
+    assert seen >= 16 * 4 * 2
 
 
 def test_backward_student_kernels(kernels):
